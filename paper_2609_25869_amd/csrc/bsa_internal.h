@@ -1,0 +1,109 @@
+// Internal declarations shared by the host runtime and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace bsa {
+
+constexpr int kHeadDim = 128;
+
+// One workgroup task (Section 4.3): a contiguous slice [tile_begin, tile_end)
+// of the active KV tiles of physical query tile `pq` of head `bh`
+// (= b * heads + h).  `split` is the slice's ordinal among the row's `nsplit`
+// slices; nsplit > 1 means the row is reduced by Split-K.
+struct Task {
+  int32_t bh, pq, tile_begin, tile_end, split, nsplit, pad0, pad1;
+};
+static_assert(sizeof(Task) == 32, "Task is 32 bytes");
+
+// Per-head facts for the mask kernels.
+struct HeadDesc {
+  int64_t mask_off;  // offset of the head's mask inside one batch
+  int32_t nqb, nkb;  // logical block grid
+  int32_t seg;       // geometry segment
+  int32_t pad;
+};
+
+// Device-side statistics of one segment (integer atomics only).
+struct SegStats {
+  unsigned long long nnz, run_blocks, max_row_nnz, pad;
+};
+
+struct MaskStateArgs {
+  const uint8_t* mask;
+  int64_t stride_b;
+  const HeadDesc* heads;
+  const int64_t* row_base;  // [B*H + 1], logical rows of (b, h) start here
+  int32_t H, nbh;
+  int64_t R;
+  int32_t* counts;          // [R]   (count pass)
+  const int64_t* row_ptr;   // [R+1] (fill pass)
+  int32_t* col_idx;         // [nnz] (fill pass)
+  SegStats* seg_stats;      // [nseg]
+  unsigned long long* bh_nnz;  // [B*H]
+};
+
+struct MapArgs {
+  const uint8_t* mask;
+  int64_t stride_b;
+  const HeadDesc* heads;
+  const int32_t* seg_heads;  // heads of the segment, ascending
+  int32_t nsh, H;
+  int32_t npq, npk;          // physical grid of one head
+  int32_t nqb, nkb;          // logical grid of one head
+  int32_t gq, gkv, rq, rkv;  // members per tile / tiles per block along Q and KV
+  int64_t Rp;                // physical rows of the segment = B * nsh * npq
+  int32_t* counts;           // count pass
+  const int64_t* tile_ptr;   // fill pass
+  int32_t* tile_kv;
+  uint64_t* member;          // may be null (no membership metadata)
+};
+
+struct TaskArgs {
+  const int64_t* tile_ptr;   // physical (or, for Direct, logical) row offsets
+  const int64_t* row_base;   // logical row base per (b, h); used when direct
+  const int32_t* seg_heads;
+  int32_t nsh, H, npq, split;
+  int32_t direct;
+  int64_t Rp;
+  int32_t* counts;           // count pass (split > 1)
+  const int64_t* task_ptr;   // fill pass (split > 1), null when split == 1
+  Task* tasks;
+};
+
+struct AttnArgs {
+  const Task* tasks;
+  int32_t ntasks;              // exact count, or an upper bound when ntasks_dev is set
+  const int64_t* ntasks_dev;   // device count (may be null)
+  const int32_t* kv_tile;
+  const uint64_t* member;      // null: every tile is fully active
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* o;
+  float* lse;                  // may be null
+  float* ws;                   // Split-K partial states (may be null when no row splits)
+  const uint16_t* zero_page;   // 256 zero bytes, read for K/V rows past the sequence end
+  int64_t qs0, qs1, qs2, ks0, ks1, ks2, vs0, vs1, vs2, os0, os1, os2;
+  int32_t H, Nq, Nkv;
+  int32_t bq_shift, bkv_shift;  // log2 of the logical block sizes
+  int32_t gq, gkv;              // membership grid of a tile
+  float scale_log2;             // log2(e) / sqrt(d)
+};
+
+// Kernel launchers (defined in the .hip files).
+hipError_t launch_mask_count(const MaskStateArgs& a, hipStream_t s);
+hipError_t launch_mask_fill(const MaskStateArgs& a, hipStream_t s);
+hipError_t launch_scan_i32(const int32_t* in, int64_t* out, int64_t n, int64_t* block_tmp, hipStream_t s);
+int64_t scan_tmp_elems(int64_t n);
+hipError_t launch_map_count(const MapArgs& a, hipStream_t s);
+hipError_t launch_map_fill(const MapArgs& a, hipStream_t s);
+hipError_t launch_task_count(const TaskArgs& a, hipStream_t s);
+hipError_t launch_task_fill(const TaskArgs& a, hipStream_t s);
+hipError_t launch_attention(int tq, int tkv, const AttnArgs& a, hipStream_t s);
+bool attention_variant_exists(int tq, int tkv);
+hipError_t launch_splitk_merge(int tq, const AttnArgs& a, hipStream_t s);
+
+}  // namespace bsa

@@ -1,0 +1,324 @@
+// Native catalog, Eligible(P, R), base plans, the plan-table artifact and the
+// online lookup of Algorithm 2 (host code, no GPU calls).
+#include "catalog.h"
+
+#include <cctype>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+
+namespace bsa {
+
+namespace {
+
+std::vector<CatalogEntry> build_catalog() {
+  // id = ((tq index) * 2 + tkv index) * 4 + split index
+  const int tqs[] = {64, 128, 256};
+  const int tkvs[] = {32, 64};
+  const int splits[] = {1, 2, 4, 8};
+  std::vector<CatalogEntry> out;
+  int id = 0;
+  for (int tq : tqs)
+    for (int tkv : tkvs)
+      for (int s : splits) out.push_back(CatalogEntry{id++, tq, tkv, s, 2, tq / 32});
+  return out;
+}
+
+bool nests(int32_t t, int32_t b) { return t > 0 && b > 0 && (t % b == 0 || b % t == 0); }
+
+bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+}  // namespace
+
+const std::vector<CatalogEntry>& catalog() {
+  static const std::vector<CatalogEntry> c = build_catalog();
+  return c;
+}
+
+const CatalogEntry* catalog_find(int32_t id) {
+  const auto& c = catalog();
+  if (id < 0 || id >= (int32_t)c.size()) return nullptr;
+  return &c[id];
+}
+
+int mapping_kind(int32_t bq, int32_t bkv, int32_t tq, int32_t tkv) {
+  if (tq == bq && tkv == bkv) return 0;
+  if (tq >= bq && tkv >= bkv) return 1;
+  if (tq <= bq && tkv <= bkv) return 2;
+  return 3;
+}
+
+const char* ineligible_reason(const CatalogEntry& e, int32_t bq, int32_t bkv, const bsa_shapes& s) {
+  if (s.dtype != BSA_DTYPE_BF16) return "only bfloat16 tensors are implemented";
+  if (s.head_dim != 128) return "only head_dim 128 is implemented";
+  const int64_t* strides[] = {s.q_stride, s.k_stride, s.v_stride, s.o_stride};
+  for (const int64_t* st : strides)
+    for (int i = 0; i < 3; ++i)
+      if (st[i] < 0 || st[i] % 8 != 0) return "strides must be non-negative multiples of 8 elements (16 bytes)";
+  if (!nests(e.tq, bq)) return "query tile and query block do not nest";
+  if (!nests(e.tkv, bkv)) return "KV tile and KV block do not nest";
+  const int64_t gq = e.tq >= bq ? e.tq / bq : 1, gkv = e.tkv >= bkv ? e.tkv / bkv : 1;
+  if (gq * gkv > 64) return "coarsened tile has more than 64 member blocks";
+  if ((gq > 1 && !is_pow2(bq)) || (gkv > 1 && !is_pow2(bkv))) return "coarsened blocks must be powers of two";
+  if (e.split < 1) return "bad split";
+  return nullptr;
+}
+
+int32_t base_plan(int32_t bq, int32_t bkv) {
+  bsa_shapes s{};
+  s.head_dim = 128;
+  s.dtype = BSA_DTYPE_BF16;
+  int32_t best = -1;
+  double best_dq = 0, best_dk = 0;
+  for (const auto& e : catalog()) {
+    if (e.split != 1 || ineligible_reason(e, bq, bkv, s)) continue;
+    const double dq = std::fabs(std::log2((double)e.tq) - std::log2((double)bq));
+    const double dk = std::fabs(std::log2((double)e.tkv) - std::log2((double)bkv));
+    if (best < 0 || dq + dk < best_dq + best_dk || (dq + dk == best_dq + best_dk && dq < best_dq)) {
+      best = e.id;
+      best_dq = dq;
+      best_dk = dk;
+    }
+  }
+  return best;
+}
+
+// ---------------------------------------------------------------------------
+// Minimal JSON reader for the artifact (objects, arrays, numbers, strings,
+// true/false/null).
+
+namespace {
+
+struct JVal {
+  enum Kind { kNull, kBool, kNum, kStr, kArr, kObj } kind = kNull;
+  double num = 0;
+  bool b = false;
+  std::string str;
+  std::vector<JVal> arr;
+  std::vector<std::pair<std::string, JVal>> obj;
+  const JVal* get(const char* key) const {
+    for (const auto& kv : obj)
+      if (kv.first == key) return &kv.second;
+    return nullptr;
+  }
+};
+
+struct JParser {
+  const std::string& t;
+  size_t i = 0;
+  std::string err;
+  explicit JParser(const std::string& text) : t(text) {}
+  void ws() {
+    while (i < t.size() && std::isspace((unsigned char)t[i])) ++i;
+  }
+  bool fail(const char* m) {
+    if (err.empty()) err = std::string(m) + " at offset " + std::to_string(i);
+    return false;
+  }
+  bool str(std::string* out) {
+    if (t[i] != '"') return fail("expected string");
+    ++i;
+    out->clear();
+    while (i < t.size() && t[i] != '"') {
+      if (t[i] == '\\') {
+        ++i;
+        if (i >= t.size()) return fail("bad escape");
+        char c = t[i];
+        out->push_back(c == 'n' ? '\n' : c == 't' ? '\t' : c);
+      } else {
+        out->push_back(t[i]);
+      }
+      ++i;
+    }
+    if (i >= t.size()) return fail("unterminated string");
+    ++i;
+    return true;
+  }
+  bool val(JVal* v, int depth) {
+    if (depth > 64) return fail("nesting too deep");
+    ws();
+    if (i >= t.size()) return fail("unexpected end");
+    char c = t[i];
+    if (c == '{') {
+      v->kind = JVal::kObj;
+      ++i;
+      ws();
+      if (i < t.size() && t[i] == '}') { ++i; return true; }
+      for (;;) {
+        ws();
+        std::string k;
+        if (!str(&k)) return false;
+        ws();
+        if (i >= t.size() || t[i] != ':') return fail("expected ':'");
+        ++i;
+        JVal x;
+        if (!val(&x, depth + 1)) return false;
+        v->obj.emplace_back(std::move(k), std::move(x));
+        ws();
+        if (i < t.size() && t[i] == ',') { ++i; continue; }
+        if (i < t.size() && t[i] == '}') { ++i; return true; }
+        return fail("expected ',' or '}'");
+      }
+    }
+    if (c == '[') {
+      v->kind = JVal::kArr;
+      ++i;
+      ws();
+      if (i < t.size() && t[i] == ']') { ++i; return true; }
+      for (;;) {
+        JVal x;
+        if (!val(&x, depth + 1)) return false;
+        v->arr.push_back(std::move(x));
+        ws();
+        if (i < t.size() && t[i] == ',') { ++i; continue; }
+        if (i < t.size() && t[i] == ']') { ++i; return true; }
+        return fail("expected ',' or ']'");
+      }
+    }
+    if (c == '"') {
+      v->kind = JVal::kStr;
+      return str(&v->str);
+    }
+    if (t.compare(i, 4, "true") == 0) { v->kind = JVal::kBool; v->b = true; i += 4; return true; }
+    if (t.compare(i, 5, "false") == 0) { v->kind = JVal::kBool; i += 5; return true; }
+    if (t.compare(i, 4, "null") == 0) { v->kind = JVal::kNull; i += 4; return true; }
+    const char* s = t.c_str() + i;
+    char* e = nullptr;
+    double d = std::strtod(s, &e);
+    if (e == s) return fail("unexpected character");
+    v->kind = JVal::kNum;
+    v->num = d;
+    i += (size_t)(e - s);
+    return true;
+  }
+};
+
+bool as_int_list(const JVal* v, std::vector<int64_t>* out) {
+  if (!v || v->kind != JVal::kArr) return false;
+  out->clear();
+  for (const auto& x : v->arr) {
+    if (x.kind != JVal::kNum || x.num != std::floor(x.num)) return false;
+    out->push_back((int64_t)x.num);
+  }
+  return true;
+}
+
+const char* kRatioFeatures[] = {"density", "run_coverage"};
+const char* kIntFeatures[] = {"seq_q", "seq_kv", "batch_heads"};
+
+bool known_feature(const std::string& n) {
+  for (const char* f : kRatioFeatures)
+    if (n == f) return true;
+  for (const char* f : kIntFeatures)
+    if (n == f) return true;
+  return false;
+}
+
+}  // namespace
+
+bool lut_parse(const std::string& text, Lut* out, std::string* err) {
+  JParser p(text);
+  JVal root;
+  if (!p.val(&root, 0)) { *err = "malformed JSON: " + p.err; return false; }
+  p.ws();
+  if (p.i != text.size()) { *err = "trailing characters after the artifact"; return false; }
+  if (root.kind != JVal::kObj) { *err = "artifact is not a JSON object"; return false; }
+  const JVal* fmt = root.get("format");
+  if (!fmt || fmt->kind != JVal::kStr || fmt->str != "bsa-plan-table") { *err = "not a bsa-plan-table artifact"; return false; }
+  const JVal* ver = root.get("version");
+  if (!ver || ver->kind != JVal::kNum || (int)ver->num != 1) { *err = "unsupported artifact version"; return false; }
+  out->version = 1;
+  const JVal* arch = root.get("arch");
+  if (!arch || arch->kind != JVal::kStr || arch->str != "gfx950") { *err = "artifact is not for gfx950"; return false; }
+  out->arch = arch->str;
+  // the catalog inside the artifact must match the library's catalog
+  const JVal* cat = root.get("catalog");
+  if (!cat || cat->kind != JVal::kArr || cat->arr.size() != catalog().size()) {
+    *err = "artifact catalog does not match this library";
+    return false;
+  }
+  for (size_t k = 0; k < cat->arr.size(); ++k) {
+    std::vector<int64_t> e;
+    if (!as_int_list(&cat->arr[k], &e) || e.size() != 6) { *err = "bad catalog entry"; return false; }
+    const CatalogEntry& c = catalog()[k];
+    if (e[0] != c.id || e[1] != c.tq || e[2] != c.tkv || e[3] != c.split || e[4] != c.stages || e[5] != c.waves) {
+      *err = "artifact catalog entry " + std::to_string(k) + " does not match this library";
+      return false;
+    }
+  }
+  const JVal* schema = root.get("schema");
+  if (!schema || schema->kind != JVal::kArr) { *err = "missing feature schema"; return false; }
+  out->feature_names.clear();
+  out->feature_edges.clear();
+  for (const auto& f : schema->arr) {
+    if (f.kind != JVal::kArr || f.arr.size() != 2 || f.arr[0].kind != JVal::kStr) { *err = "bad schema entry"; return false; }
+    if (!known_feature(f.arr[0].str)) { *err = "unknown feature " + f.arr[0].str; return false; }
+    std::vector<int64_t> edges;
+    if (!as_int_list(&f.arr[1], &edges)) { *err = "bad bucket edges"; return false; }
+    for (size_t k = 1; k < edges.size(); ++k)
+      if (edges[k] <= edges[k - 1]) { *err = "bucket edges must increase"; return false; }
+    out->feature_names.push_back(f.arr[0].str);
+    out->feature_edges.push_back(edges);
+  }
+  const JVal* regimes = root.get("regimes");
+  if (!regimes || regimes->kind != JVal::kArr) { *err = "missing regimes"; return false; }
+  out->table.clear();
+  for (const auto& r : regimes->arr) {
+    std::vector<int64_t> key, bucket, ranking;
+    if (r.kind != JVal::kObj || !as_int_list(r.get("key"), &key) || key.size() != 4 ||
+        !as_int_list(r.get("bucket"), &bucket) || bucket.size() != out->feature_names.size() ||
+        !as_int_list(r.get("ranking"), &ranking) || ranking.empty()) {
+      *err = "bad regime entry";
+      return false;
+    }
+    std::vector<int32_t> rk;
+    for (int64_t id : ranking) {
+      if (!catalog_find((int32_t)id)) { *err = "ranking names an unknown plan"; return false; }
+      rk.push_back((int32_t)id);
+    }
+    out->table[key][bucket] = rk;
+  }
+  return true;
+}
+
+std::vector<int64_t> lut_bucket(const Lut& lut, const bsa_regime_query& z) {
+  std::vector<int64_t> b;
+  for (size_t f = 0; f < lut.feature_names.size(); ++f) {
+    const std::string& n = lut.feature_names[f];
+    const auto& edges = lut.feature_edges[f];
+    int64_t idx = 0;
+    if (n == "density" || n == "run_coverage") {
+      int64_t num = n == "density" ? z.nnz : z.run_blocks;
+      int64_t den = n == "density" ? z.blocks : z.nnz;
+      if (den <= 0) { num = 0; den = 1; }
+      for (int64_t e : edges)
+        if ((__int128)num * 10000 >= (__int128)e * den) ++idx;
+    } else {
+      const int64_t v = n == "seq_q" ? z.seq_q : n == "seq_kv" ? z.seq_kv : z.batch_heads;
+      for (int64_t e : edges)
+        if (v >= e) ++idx;
+    }
+    b.push_back(idx);
+  }
+  return b;
+}
+
+std::vector<int32_t> lut_ranking(const Lut* lut, const bsa_regime_query& z, bool* hit) {
+  *hit = false;
+  if (lut) {
+    const std::vector<int64_t> key{z.bq, z.bkv, z.dtype, z.head_dim};
+    auto it = lut->table.find(key);
+    if (it != lut->table.end()) {
+      auto jt = it->second.find(lut_bucket(*lut, z));
+      if (jt != it->second.end()) {
+        *hit = true;
+        return jt->second;
+      }
+    }
+  }
+  const int32_t base = base_plan(z.bq, z.bkv);
+  if (base < 0) return {};
+  return {base};
+}
+
+}  // namespace bsa

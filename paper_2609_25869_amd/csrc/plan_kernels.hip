@@ -1,0 +1,297 @@
+// Planning kernels for gfx950: the shared mask state mu(M) (block-CSR and
+// mask statistics, Section 5.2), the physical mapping of the selected plan
+// (Section 4.2) and its task organisation (Section 4.3).
+//
+// Row-oriented kernels give one 64-lane wavefront to one row.  A row is read
+// 64 columns per step with coalesced byte loads; ballot masks carry the
+// activity of the step, so counting, run detection and compaction are scalar
+// bit operations on one 64-bit word.
+#include "bsa_internal.h"
+
+namespace bsa {
+
+namespace {
+
+constexpr int kRowsPerBlock = 4;  // wavefronts (rows) per 256-thread workgroup
+
+__device__ inline int find_bh(const int64_t* row_base, int nbh, int64_t r) {
+  int lo = 0, hi = nbh;  // row_base[lo] <= r < row_base[hi]
+  while (hi - lo > 1) {
+    int mid = (lo + hi) >> 1;
+    if (row_base[mid] <= r) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+__device__ inline uint64_t lanes_below(int lane) { return (lane == 0) ? 0ull : ((~0ull) >> (64 - lane)); }
+
+// Logical rows: count (with statistics) or fill the block-CSR columns.
+template <bool kFill>
+__global__ __launch_bounds__(256) void mask_rows_kernel(MaskStateArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (r >= a.R) return;
+  const int bh = find_bh(a.row_base, a.nbh, r);
+  const int b = bh / a.H, h = bh - b * a.H;
+  const HeadDesc hd = a.heads[h];
+  const int64_t qb = r - a.row_base[bh];
+  const uint8_t* row = a.mask + b * a.stride_b + hd.mask_off + qb * (int64_t)hd.nkb;
+  const int64_t out_base = kFill ? a.row_ptr[r] : 0;
+  int64_t nnz = 0, run = 0;
+  uint64_t carry = 0;  // activity of the column just before the current step
+  for (int c0 = 0; c0 < hd.nkb; c0 += 64) {
+    const int c = c0 + lane;
+    const bool act = (c < hd.nkb) && row[c] != 0;
+    const uint64_t bits = __ballot(act);
+    if (kFill) {
+      if (act) a.col_idx[out_base + nnz + __popcll(bits & lanes_below(lane))] = c;
+    } else {
+      const uint64_t next = (c0 + 64 < hd.nkb && row[c0 + 64] != 0) ? 1ull : 0ull;
+      const uint64_t left = (bits << 1) | carry;        // column c-1 active
+      const uint64_t right = (bits >> 1) | (next << 63);  // column c+1 active
+      run += __popcll(bits & (left | right));
+      carry = bits >> 63;
+    }
+    nnz += __popcll(bits);
+  }
+  if (!kFill && lane == 0) {
+    a.counts[r] = (int32_t)nnz;
+    SegStats* st = a.seg_stats + hd.seg;
+    atomicAdd(&st->nnz, (unsigned long long)nnz);
+    atomicAdd(&st->run_blocks, (unsigned long long)run);
+    atomicMax(&st->max_row_nnz, (unsigned long long)nnz);
+    atomicAdd(a.bh_nnz + bh, (unsigned long long)nnz);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Exclusive scan int32 -> int64 with the total in out[n]; three passes:
+// per-block sums, a one-block scan of those sums, per-block rescans.
+constexpr int kScanThreads = 256;
+constexpr int kScanItems = 8;
+constexpr int kScanTile = kScanThreads * kScanItems;
+
+__device__ inline int64_t block_exclusive_scan(int64_t x, int64_t* total) {
+  __shared__ int64_t wsum[kScanThreads / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int64_t incl = x;
+  for (int off = 1; off < 64; off <<= 1) {
+    int64_t y = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += y;
+  }
+  if (lane == 63) wsum[w] = incl;
+  __syncthreads();
+  int64_t before = 0, all = 0;
+  for (int i = 0; i < kScanThreads / 64; ++i) {
+    if (i < w) before += wsum[i];
+    all += wsum[i];
+  }
+  __syncthreads();
+  *total = all;
+  return before + incl - x;
+}
+
+__global__ __launch_bounds__(kScanThreads) void scan_block_sums(const int32_t* in, int64_t n, int64_t* sums) {
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + threadIdx.x * kScanItems;
+  int64_t s = 0;
+  for (int i = 0; i < kScanItems; ++i)
+    if (base + i < n) s += in[base + i];
+  int64_t total;
+  (void)block_exclusive_scan(s, &total);
+  if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(kScanThreads) void scan_sums(int64_t* sums, int64_t nblocks) {
+  int64_t carry = 0;
+  for (int64_t base = 0; base < nblocks; base += kScanThreads) {
+    const int64_t i = base + threadIdx.x;
+    const int64_t x = i < nblocks ? sums[i] : 0;
+    int64_t total;
+    const int64_t ex = block_exclusive_scan(x, &total);
+    if (i < nblocks) sums[i] = carry + ex;
+    carry += total;
+  }
+}
+
+__global__ __launch_bounds__(kScanThreads) void scan_apply(const int32_t* in, int64_t n, const int64_t* sums,
+                                                           int64_t* out) {
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + threadIdx.x * kScanItems;
+  int64_t v[kScanItems];
+  int64_t s = 0;
+  for (int i = 0; i < kScanItems; ++i) {
+    v[i] = (base + i < n) ? in[base + i] : 0;
+    s += v[i];
+  }
+  int64_t total;
+  int64_t run = sums[blockIdx.x] + block_exclusive_scan(s, &total);
+  for (int i = 0; i < kScanItems; ++i) {
+    if (base + i < n) out[base + i] = run;
+    run += v[i];
+  }
+  if (base < n && base + kScanItems >= n) out[n] = run;  // the thread holding the last element
+}
+
+__global__ void zero_i64(int64_t* out) {
+  if (threadIdx.x == 0) out[0] = 0;
+}
+
+// ---------------------------------------------------------------------------
+// Physical mapping of one geometry segment (Section 4.2): tile (pq, pk) is
+// active iff one of its member logical blocks is; bit a*gkv + c records
+// member (a, c) for Coarsened tiles.
+template <bool kFill>
+__global__ __launch_bounds__(256) void map_rows_kernel(MapArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t rp = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (rp >= a.Rp) return;
+  const int64_t per_b = (int64_t)a.nsh * a.npq;
+  const int b = (int)(rp / per_b);
+  const int j = (int)((rp / a.npq) % a.nsh);
+  const int pq = (int)(rp % a.npq);
+  const int h = a.seg_heads[j];
+  const HeadDesc hd = a.heads[h];
+  const uint8_t* mh = a.mask + b * a.stride_b + hd.mask_off;
+  int qb0, nqm;
+  if (a.gq > 1 || a.rq == 1) {
+    qb0 = pq * a.gq;
+    nqm = min(a.gq, a.nqb - qb0);
+  } else {
+    qb0 = pq / a.rq;
+    nqm = 1;
+  }
+  const int64_t out_base = kFill ? a.tile_ptr[rp] : 0;
+  int64_t n = 0;
+  for (int p0 = 0; p0 < a.npk; p0 += 64) {
+    const int pk = p0 + lane;
+    uint64_t bits = 0;
+    if (pk < a.npk) {
+      int kb0, nkm;
+      if (a.gkv > 1 || a.rkv == 1) {
+        kb0 = pk * a.gkv;
+        nkm = min(a.gkv, a.nkb - kb0);
+      } else {
+        kb0 = pk / a.rkv;
+        nkm = 1;
+      }
+      for (int ai = 0; ai < nqm; ++ai) {
+        const uint8_t* row = mh + (int64_t)(qb0 + ai) * a.nkb + kb0;
+        for (int ci = 0; ci < nkm; ++ci)
+          if (row[ci]) bits |= 1ull << (ai * a.gkv + ci);
+      }
+    }
+    const bool act = bits != 0;
+    const uint64_t ball = __ballot(act);
+    if (kFill && act) {
+      const int64_t pos = out_base + n + __popcll(ball & lanes_below(lane));
+      a.tile_kv[pos] = pk;
+      if (a.member) a.member[pos] = bits;
+    }
+    n += __popcll(ball);
+  }
+  if (!kFill && lane == 0) a.counts[rp] = (int32_t)n;
+}
+
+// ---------------------------------------------------------------------------
+// Task organisation (Section 4.3): physical row rs of the segment is cut into
+// `split` contiguous slices [floor(s*n/S), floor((s+1)*n/S)); empty slices
+// are dropped; a row without active tiles keeps one empty task.
+__device__ inline void task_row(const TaskArgs& a, int64_t rs, int* bh, int* pq, int64_t* lo, int64_t* hi) {
+  const int64_t per_b = (int64_t)a.nsh * a.npq;
+  const int b = (int)(rs / per_b);
+  const int j = (int)((rs / a.npq) % a.nsh);
+  *pq = (int)(rs % a.npq);
+  *bh = b * a.H + a.seg_heads[j];
+  const int64_t row = a.direct ? a.row_base[*bh] + *pq : rs;
+  *lo = a.tile_ptr[row];
+  *hi = a.tile_ptr[row + 1];
+}
+
+__global__ __launch_bounds__(256) void task_count_kernel(TaskArgs a) {
+  const int64_t rs = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (rs >= a.Rp) return;
+  int bh, pq;
+  int64_t lo, hi;
+  task_row(a, rs, &bh, &pq, &lo, &hi);
+  const int64_t n = hi - lo;
+  a.counts[rs] = (int32_t)(n == 0 ? 1 : (n < a.split ? n : a.split));
+}
+
+__global__ __launch_bounds__(256) void task_fill_kernel(TaskArgs a) {
+  const int64_t rs = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (rs >= a.Rp) return;
+  int bh, pq;
+  int64_t lo, hi;
+  task_row(a, rs, &bh, &pq, &lo, &hi);
+  const int64_t n = hi - lo;
+  int64_t out = a.task_ptr ? a.task_ptr[rs] : rs;
+  if (n == 0 || a.split == 1) {
+    Task t{bh, pq, (int32_t)lo, (int32_t)hi, 0, 1, 0, 0};
+    a.tasks[out] = t;
+    return;
+  }
+  const int nsplit = (int)(n < a.split ? n : a.split);
+  int s_out = 0;
+  for (int s = 0; s < a.split; ++s) {
+    const int64_t b0 = lo + (s * n) / a.split, b1 = lo + ((s + 1) * n) / a.split;
+    if (b1 == b0) continue;
+    Task t{bh, pq, (int32_t)b0, (int32_t)b1, s_out, nsplit, 0, 0};
+    a.tasks[out + s_out] = t;
+    ++s_out;
+  }
+}
+
+inline unsigned grid_for(int64_t rows, int per_block) { return (unsigned)((rows + per_block - 1) / per_block); }
+
+}  // namespace
+
+hipError_t launch_mask_count(const MaskStateArgs& a, hipStream_t s) {
+  if (a.R == 0) return hipSuccess;
+  hipLaunchKernelGGL(mask_rows_kernel<false>, dim3(grid_for(a.R, kRowsPerBlock)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_mask_fill(const MaskStateArgs& a, hipStream_t s) {
+  if (a.R == 0) return hipSuccess;
+  hipLaunchKernelGGL(mask_rows_kernel<true>, dim3(grid_for(a.R, kRowsPerBlock)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+int64_t scan_tmp_elems(int64_t n) { return (n + kScanTile - 1) / kScanTile + 1; }
+
+hipError_t launch_scan_i32(const int32_t* in, int64_t* out, int64_t n, int64_t* block_tmp, hipStream_t s) {
+  if (n == 0) {
+    hipLaunchKernelGGL(zero_i64, dim3(1), dim3(64), 0, s, out);
+    return hipGetLastError();
+  }
+  const int64_t nb = (n + kScanTile - 1) / kScanTile;
+  hipLaunchKernelGGL(scan_block_sums, dim3((unsigned)nb), dim3(kScanThreads), 0, s, in, n, block_tmp);
+  hipLaunchKernelGGL(scan_sums, dim3(1), dim3(kScanThreads), 0, s, block_tmp, nb);
+  hipLaunchKernelGGL(scan_apply, dim3((unsigned)nb), dim3(kScanThreads), 0, s, in, n, block_tmp, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_map_count(const MapArgs& a, hipStream_t s) {
+  if (a.Rp == 0) return hipSuccess;
+  hipLaunchKernelGGL(map_rows_kernel<false>, dim3(grid_for(a.Rp, kRowsPerBlock)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_map_fill(const MapArgs& a, hipStream_t s) {
+  if (a.Rp == 0) return hipSuccess;
+  hipLaunchKernelGGL(map_rows_kernel<true>, dim3(grid_for(a.Rp, kRowsPerBlock)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_task_count(const TaskArgs& a, hipStream_t s) {
+  if (a.Rp == 0) return hipSuccess;
+  hipLaunchKernelGGL(task_count_kernel, dim3(grid_for(a.Rp, 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_task_fill(const TaskArgs& a, hipStream_t s) {
+  if (a.Rp == 0) return hipSuccess;
+  hipLaunchKernelGGL(task_fill_kernel, dim3(grid_for(a.Rp, 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace bsa
