@@ -1,6 +1,9 @@
 // Block-sparse attention forward for gfx950 (CDNA4): one workgroup per task,
 // NWAVES wavefronts of 32 query rows each (T_Q = 32 * NWAVES), K/V tiles of
-// TKV tokens streamed through a two-stage LDS ring (Sections 2.3, 4.2, 4.3).
+// TKV tokens streamed through LDS rings of STAGES slots (pipeline depth,
+// Sections 2.3, 4.2, 4.3).  The loop is software pipelined: the scores of
+// tile t+1 (MFMA) are computed while the probabilities of tile t (VALU) are
+// formed, then O accumulates P V of tile t.
 //
 // Layout of the work inside a wavefront
 //   The score tile is computed transposed, S^T = K Q^T, with
@@ -60,10 +63,6 @@ __device__ inline i16x4 lds_read_tr(const uint8_t* p) {
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// wait for this wave's outstanding vector-memory operations (the LDS DMA of
-// the next tile); gfx9 s_waitcnt encoding with expcnt and lgkmcnt at maximum
-__device__ inline void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-
 template <int NWAVES, int TKV>
 struct Cfg {
   static constexpr int kThreads = 64 * NWAVES;
@@ -82,16 +81,61 @@ __device__ inline int64_t task_of_slot(int64_t slot, int64_t nt) {
   return t < nt ? t : -1;
 }
 
-template <int NWAVES, int TKV>
+// Value of the same register in lane l ^ 32 (the other half of the wave).
+__device__ inline float other_half(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  // lanes 0-31 find the partner in r[1], lanes 32-63 in r[0]; the other entry is x itself
+  return (threadIdx.x & 32) ? __uint_as_float(r[0]) : __uint_as_float(r[1]);
+}
+
+// The running maximum is only raised when a tile's maximum exceeds it by more
+// than kTau (log2 units).  Until then probabilities are computed against the
+// old reference and stay below 2^kTau, which fp32 sums and bf16 P hold
+// exactly as well; the rescale of O is skipped for most tiles.
+constexpr float kTau = 8.0f;
+
+// Wait until at most N of this wave's vector-memory operations (the LDS DMA
+// of younger tiles) are outstanding and all of its LDS reads have retired
+// (gfx9 s_waitcnt encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4 at its
+// maximum, lgkmcnt 11:8 = 0).
+template <int N>
+__device__ inline void wait_vm_lgkm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0070 | (N & 15) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier without a memory fence: LDS writes made by the DMA are
+// complete once vmcnt says so, and a fence here would also drain the
+// prefetches that are meant to stay in flight.  The empty asm statements
+// keep the compiler from moving memory accesses across the barrier.
+__device__ inline void block_sync() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int NWAVES, int TKV, int STAGES>
 __global__ __launch_bounds__(64 * NWAVES) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_kernel(AttnArgs a) {
   using C = Cfg<NWAVES, TKV>;
-  // two pipeline stages, each a K tile and a V tile (separate arrays so the
-  // compiler can tell the stage being filled from the stage being read)
-  __shared__ __attribute__((aligned(1024))) uint8_t k0s[C::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t v0s[C::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t k1s[C::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t v1s[C::kTileBytes];
+  constexpr int kNKB = C::kNKB;
+  static_assert(STAGES == 2 || STAGES == 4, "ring depth");
+  // A ring of STAGES slots; slot j holds a K tile and a V tile.  Iteration t
+  // consumes slot (t+1) % STAGES, which holds K of tile t+1 (scores of the
+  // next tile) and V of tile t (this tile's output), and refills slot
+  // t % STAGES (consumed by iteration t-1) with K of tile t+STAGES and V of
+  // tile t+STAGES-1, so every load has STAGES-2 whole iterations plus the
+  // current one to arrive.  Each slot is its own array: the compiler then
+  // sees that reads of one slot never alias the DMA filling another and
+  // keeps those loads in flight.
+  constexpr int kSlotBytes = 2 * C::kTileBytes;
+  constexpr int kSpareBytes = STAGES > 2 ? kSlotBytes : 16;
+  __shared__ __attribute__((aligned(1024))) uint8_t ring0[kSlotBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t ring1[kSlotBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t ring2[kSpareBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t ring3[kSpareBytes];
+  auto kslot = [&](int i) -> uint8_t* { return i == 0 ? ring0 : i == 1 ? ring1 : i == 2 ? ring2 : ring3; };
+  auto vslot = [&](int i) -> uint8_t* { return kslot(i) + C::kTileBytes; };
 
   const int64_t nt = a.ntasks_dev ? *a.ntasks_dev : a.ntasks;
   const int64_t ti = task_of_slot(blockIdx.x, nt);
@@ -121,38 +165,60 @@ void attn_fwd_kernel(AttnArgs a) {
     }
   }
 
-  const uint16_t* kbase = a.k + b * a.ks0 + h * a.ks1;
-  const uint16_t* vbase = a.v + b * a.vs0 + h * a.vs1;
+  // The task's tile list and membership bits are read through the scalar
+  // cache (constant address space): vector loads would be counted together
+  // with the in-flight K/V loads and force them to drain.
+  typedef const __attribute__((address_space(4))) int32_t* ci32p;
+  typedef const __attribute__((address_space(4))) uint64_t* cu64p;
+  const int tb = task.tile_begin;
+  const int nkv_tiles = task.tile_end - tb;
+  ci32p kvt = (ci32p)(a.kv_tile + tb);
+  cu64p mbits = a.member ? (cu64p)(a.member + tb) : nullptr;
 
-  // Direct global -> LDS loads: one instruction moves 64 lanes x 16 bytes =
-  // 4 token rows into 1 KB of LDS, lane i landing at byte 16 * i.  Lane i of
-  // load j therefore owns LDS row rr = 4 * (w + j * NWAVES) + i / 16 and
-  // physical chunk i % 16, and fetches the logical chunk that the swizzle
-  // places there.  Rows past the sequence end read a zero page.
+  // ---- direct global -> LDS loads
+  // One instruction moves 64 lanes x 16 bytes = 4 token rows into 1 KB of
+  // LDS, lane i landing at byte 16 * i.  Lane i of load j owns LDS row
+  // rr = 4 * (w + j * NWAVES) + i / 16 and physical chunk i % 16, and fetches
+  // the logical chunk that the swizzle places there.  Addresses are a
+  // wave-uniform tile base plus a per-lane 32-bit offset fixed for the task.
   constexpr int kLoadsPerWave = TKV / (4 * NWAVES);
   static_assert(kLoadsPerWave >= 1 && TKV % (4 * NWAVES) == 0, "tile rows must split over the waves");
-  int64_t src_off[kLoadsPerWave];  // element offset of this lane's chunk inside a token-row block
-  int src_row[kLoadsPerWave];
+  const char* kbase = reinterpret_cast<const char*>(a.k + b * a.ks0 + h * a.ks1);
+  const char* vbase = reinterpret_cast<const char*>(a.v + b * a.vs0 + h * a.vs1);
+  const int64_t kstride = a.ks2 * 2, vstride = a.vs2 * 2;  // bytes per token
+  uint32_t koffs[kLoadsPerWave], voffs[kLoadsPerWave];
 #pragma unroll
   for (int j = 0; j < kLoadsPerWave; ++j) {
     const int rr = 4 * (w + j * NWAVES) + (lane >> 4);
     const int ch = (lane & 15) ^ swz(rr & 15);
-    src_row[j] = rr;
-    src_off[j] = ch * 8;
+    koffs[j] = (uint32_t)(rr * kstride) + ch * 16;
+    voffs[j] = (uint32_t)(rr * vstride) + ch * 16;
   }
-  auto issue_tile = [&](int tile, uint8_t* kd, uint8_t* vd) {
-    const int kv0 = a.kv_tile[tile] * TKV;
+  // copy the TKV tokens starting at kv0 into one ring slot
+  auto dma_rows = [&](const char* base, int64_t stride, const uint32_t* offs, int kv0, uint8_t* dst_arr) {
+    const char* t0 = base + (int64_t)kv0 * stride;
+    if (kv0 + TKV <= a.Nkv) {
 #pragma unroll
-    for (int j = 0; j < kLoadsPerWave; ++j) {
-      const int tok = kv0 + src_row[j];
-      const bool ok = tok < a.Nkv;
-      const uint16_t* kp = ok ? kbase + (int64_t)tok * a.ks2 + src_off[j] : a.zero_page;
-      const uint16_t* vp = ok ? vbase + (int64_t)tok * a.vs2 + src_off[j] : a.zero_page;
-      const int dst = 1024 * (w + j * NWAVES);
-      __builtin_amdgcn_global_load_lds(kp, (__attribute__((address_space(3))) void*)(kd + dst), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(vp, (__attribute__((address_space(3))) void*)(vd + dst), 16, 0, 0);
+      for (int j = 0; j < kLoadsPerWave; ++j)
+        __builtin_amdgcn_global_load_lds(t0 + offs[j],
+                                         (__attribute__((address_space(3))) void*)(dst_arr + 1024 * (w + j * NWAVES)),
+                                         16, 0, 0);
+    } else {
+      // sequence tail: rows past the end read the zero page
+#pragma unroll
+      for (int j = 0; j < kLoadsPerWave; ++j) {
+        const int rr = 4 * (w + j * NWAVES) + (lane >> 4);
+        const void* p = (kv0 + rr < a.Nkv) ? static_cast<const void*>(t0 + offs[j])
+                                            : static_cast<const void*>(a.zero_page);
+        __builtin_amdgcn_global_load_lds(p, (__attribute__((address_space(3))) void*)(dst_arr + 1024 * (w + j * NWAVES)),
+                                         16, 0, 0);
+      }
     }
   };
+  auto dma_k = [&](int kv0, int slot) { dma_rows(kbase, kstride, koffs, kv0, kslot(slot)); };
+  auto dma_v = [&](int kv0, int slot) { dma_rows(vbase, vstride, voffs, kv0, vslot(slot)); };
+  // first token of tile t, clamped to the task's last tile
+  auto tile_kv0 = [&](int t) -> int { return kvt[t < nkv_tiles ? t : nkv_tiles - 1] * TKV; };
 
   // lane-constant LDS offsets
   const int sw = swz(lane & 15);
@@ -178,120 +244,192 @@ void attn_fwd_kernel(AttnArgs a) {
   const int mem_row = (a.gq > 1) ? (q_local >> a.bq_shift) : 0;
   const int mem_bits = a.gq * a.gkv;
   const uint64_t full = (mem_bits >= 64) ? ~0ull : ((1ull << mem_bits) - 1);
+  const float c_log2 = a.scale_log2;
 
   f32x16 o[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) o[i] = f32x16{};
   float m_run = kNegInf, l_run = 0.f;
 
-  auto step = [&](const uint8_t* ks, const uint8_t* vs, int tile) {
-    // ---- S^T = K Q^T
-    f32x16 s[C::kNKB];
-#pragma unroll
-    for (int kb = 0; kb < C::kNKB; ++kb) s[kb] = f32x16{};
-#pragma unroll
-    for (int c = 0; c < 8; ++c) {
-#pragma unroll
-      for (int kb = 0; kb < C::kNKB; ++kb) {
-        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(ks + kb * 32 * kRowBytes + koff[c]);
-        s[kb] = mfma32(ka, qf[c], s[kb]);
-      }
+  // MFMA operand stream of one iteration: units [0, kNA) are the S^T MFMAs of
+  // the next tile (A = K rows), units [kNA, kNU) the O^T MFMAs of this tile
+  // (A = V^T via transposed reads).  Operands are read two units ahead.
+  constexpr int kNA = 8 * kNKB;
+  constexpr int kNB = 4 * (TKV / 16);
+  constexpr int kNU = kNA + kNB;
+  auto load_op = [&](int u, const uint8_t* ks, const uint8_t* vs) -> bf16x8 {
+    if (u < kNA) {
+      const int c = u / kNKB, kb = u % kNKB;
+      return *reinterpret_cast<const bf16x8*>(ks + kb * 32 * kRowBytes + koff[c]);
     }
+    const int j = u - kNA, t = j / 4, dblk = j % 4;
+    const i16x4 lo = lds_read_tr(vs + t * 16 * kRowBytes + voff[0][dblk]);
+    const i16x4 hi = lds_read_tr(vs + t * 16 * kRowBytes + voff[1][dblk]);
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
 
-    // ---- mask (tile members / sequence tail), scale, row max
-    const int kv0 = a.kv_tile[tile] * TKV;
-    const uint64_t bits = a.member ? a.member[tile] : full;
-    const bool tail = kv0 + TKV > a.Nkv;
-    float mx = kNegInf;
-    if (tail || bits != full) {
-      const uint64_t rowbits = (bits >> (mem_row * a.gkv));
+  // raw scores S^T of one tile with nothing else to overlap (prologue)
+  auto qk_only = [&](const uint8_t* ks, f32x16* s) {
 #pragma unroll
-      for (int kb = 0; kb < C::kNKB; ++kb) {
+    for (int kb = 0; kb < kNKB; ++kb) s[kb] = f32x16{};
+    bf16x8 op[3];
+    op[0] = load_op(0, ks, nullptr);
+    op[1] = load_op(1, ks, nullptr);
+#pragma unroll
+    for (int u = 0; u < kNA; ++u) {
+      if (u + 2 < kNA) op[(u + 2) % 3] = load_op(u + 2, ks, nullptr);
+      s[u % kNKB] = mfma32(op[u % 3], qf[u / kNKB], s[u % kNKB]);
+    }
+  };
+
+  // entries outside the tile's active members or past the sequence end -> -inf
+  auto apply_mask = [&](f32x16* s, int kv0, uint64_t bits) {
+    if (__builtin_expect(kv0 + TKV > a.Nkv || bits != full, 0)) {
+      const uint64_t rowbits = bits >> (mem_row * a.gkv);
+      // allowed-key bitmap of this lane's row over the tile
+      uint64_t allowed = 0;
+      const int nvalid = min(TKV, a.Nkv - kv0);
+      const uint64_t tailmask = nvalid >= 64 ? ~0ull : ((1ull << nvalid) - 1);
+      if (a.gkv > 1) {
+        const int bkv = 1 << a.bkv_shift;
+        const uint64_t run = bkv >= 64 ? ~0ull : ((1ull << bkv) - 1);
+        for (int cm = 0; cm < a.gkv; ++cm)
+          if ((rowbits >> cm) & 1ull) allowed |= run << (cm * bkv);
+      } else {
+        allowed = (rowbits & 1ull) ? ~0ull : 0ull;
+      }
+      allowed &= tailmask;
+      const uint64_t mine = allowed >> (4 * hh);
+#pragma unroll
+      for (int kb = 0; kb < kNKB; ++kb) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const int j = kb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-          const int c = (a.gkv > 1) ? (j >> a.bkv_shift) : 0;
-          const bool ok = (kv0 + j < a.Nkv) && ((rowbits >> c) & 1ull);
-          const float x = ok ? s[kb][i] * a.scale_log2 : kNegInf;
-          s[kb][i] = x;
-          mx = fmaxf(mx, x);
+          const int jc = kb * 32 + (i >> 2) * 8 + (i & 3);  // key index minus 4 * hh
+          s[kb][i] = ((mine >> jc) & 1ull) ? s[kb][i] : kNegInf;
         }
-      }
-    } else {
-#pragma unroll
-      for (int kb = 0; kb < C::kNKB; ++kb) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float x = s[kb][i] * a.scale_log2;
-          s[kb][i] = x;
-          mx = fmaxf(mx, x);
-        }
-      }
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-
-    // ---- online softmax update
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
-    m_run = m_new;
-    float rs = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < C::kNKB; ++kb) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = fast_exp2(s[kb][i] - m_use);
-        s[kb][i] = p;
-        rs += p;
-      }
-    }
-    l_run = l_run * alpha + rs;
-#pragma unroll
-    for (int d = 0; d < 4; ++d) o[d] *= alpha;
-
-    // ---- O^T += V^T P^T
-#pragma unroll
-    for (int t = 0; t < TKV / 16; ++t) {
-      bf16x8 pb;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) pb[e] = (__bf16)s[t >> 1][8 * (t & 1) + e];
-#pragma unroll
-      for (int dblk = 0; dblk < 4; ++dblk) {
-        const i16x4 lo = lds_read_tr(vs + t * 16 * kRowBytes + voff[0][dblk]);
-        const i16x4 hi = lds_read_tr(vs + t * 16 * kRowBytes + voff[1][dblk]);
-        const bf16x4 lo4 = __builtin_bit_cast(bf16x4, lo);
-        const bf16x4 hi4 = __builtin_bit_cast(bf16x4, hi);
-        bf16x8 va;
-        va[0] = lo4[0]; va[1] = lo4[1]; va[2] = lo4[2]; va[3] = lo4[3];
-        va[4] = hi4[0]; va[5] = hi4[1]; va[6] = hi4[2]; va[7] = hi4[3];
-        o[dblk] = mfma32(va, pb, o[dblk]);
       }
     }
   };
 
-  // two-stage ring: while one stage is consumed the next tile streams into
-  // the other; one barrier per tile
-  const int nkv_tiles = task.tile_end - task.tile_begin;
+  // One pipeline iteration over tile t (scores in s_cur): mask, row max and
+  // the rare rescale; then the S^T MFMAs of the next tile (from ks_next)
+  // interleaved with the probabilities of this tile, and the O^T MFMAs of
+  // this tile (V from vs_cur) interleaved with the rest of them.
+  auto iteration = [&](f32x16* s_cur, f32x16* s_nxt, int kv0_cur, uint64_t bits_cur, const uint8_t* ks_next,
+                       const uint8_t* vs_cur) {
+    apply_mask(s_cur, kv0_cur, bits_cur);
+
+    // row maximum of the raw scores (the scale is positive)
+    float mx = kNegInf;
+#pragma unroll
+    for (int kb = 0; kb < kNKB; ++kb) {
+#pragma unroll
+      for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(s_cur[kb][i], s_cur[kb][i + 1]));
+    }
+    mx = fmaxf(mx, other_half(mx));
+    const float mxs = mx * c_log2;
+    // raise the reference only when needed (wave-uniform branch)
+    const bool need = mxs > m_run + kTau;
+    if (__ballot(need)) {
+      const float m_new = need ? mxs : m_run;
+      const float alpha = need ? fast_exp2(m_run - m_new) : 1.f;
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int d = 0; d < 4; ++d) o[d] *= alpha;
+    }
+    const float nm = (m_run == kNegInf) ? 0.f : -m_run;
+
+#pragma unroll
+    for (int kb = 0; kb < kNKB; ++kb) s_nxt[kb] = f32x16{};
+    float ls[4] = {0.f, 0.f, 0.f, 0.f};
+    bf16x8 pb[TKV / 16];
+    // probability of element ei (chunk ei / 8, slot ei % 8 of that chunk)
+    auto prob = [&](int ei) {
+      const float p = fast_exp2(__builtin_fmaf(s_cur[ei / 16][ei % 16], c_log2, nm));
+      ls[ei & 3] += p;
+      pb[ei / 8][ei % 8] = (__bf16)p;
+    };
+    bf16x8 op[3];
+    op[0] = load_op(0, ks_next, vs_cur);
+    op[1] = load_op(1, ks_next, vs_cur);
+#pragma unroll
+    for (int u = 0; u < kNU; ++u) {
+      if (u + 2 < kNU) op[(u + 2) % 3] = load_op(u + 2, ks_next, vs_cur);
+      if (u < kNA) {
+        s_nxt[u % kNKB] = mfma32(op[u % 3], qf[u / kNKB], s_nxt[u % kNKB]);
+        prob(u);  // first half of the elements, one per unit
+      } else {
+        const int j = u - kNA;
+        o[j % 4] = mfma32(op[u % 3], pb[j / 4], o[j % 4]);
+        if (j < kNB / 2) {  // second half, two per unit
+          prob(kNA + 2 * j);
+          prob(kNA + 2 * j + 1);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    l_run += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+  };
+
+  // number of DMA instructions one iteration issues (K tile and V tile)
+  constexpr int kGroup = 2 * kLoadsPerWave;
+  constexpr int kInFlight = (STAGES - 2) * kGroup;
+
+  f32x16 sA[kNKB], sB[kNKB];
+  // scalars for the coming iteration, fetched one iteration ahead
+  int kv_next_k = 0, kv_next_v = 0, kv_cur = 0;
+  uint64_t bits_cur = full;
   if (nkv_tiles > 0) {
-    issue_tile(task.tile_begin, k0s, v0s);
-    wait_vmem();
-    __syncthreads();
+    // prologue: K of tile 0 into slot 0, then slot j <- (K of tile j, V of
+    // tile j-1) for j = 1..STAGES-1, in the order they are needed.  Ring
+    // refills are never skipped: past the end of the task they re-load its
+    // last tile into the free slot, which keeps the count of loads in flight
+    // the same on every path.
+    dma_k(tile_kv0(0), 0);
+#pragma unroll
+    for (int j = 1; j < STAGES; ++j) {
+      dma_k(tile_kv0(j), j);
+      dma_v(tile_kv0(j - 1), j);
+    }
+    kv_next_k = tile_kv0(STAGES);
+    kv_next_v = tile_kv0(STAGES - 1);
+    kv_cur = tile_kv0(0);
+    bits_cur = mbits ? mbits[0] : full;
+    // the scores of tile 0 need K0 only
+    wait_vm_lgkm<(STAGES - 1) * kGroup>();
+    block_sync();
+    qk_only(kslot(0), sA);
+    // the first iteration needs slot 1
+    wait_vm_lgkm<kInFlight>();
+    block_sync();  // every wave has read slot 0 before it is refilled
   }
-  for (int it = 0; it < nkv_tiles; it += 2) {
-    const int tile = task.tile_begin + it;
-    if (it + 1 < nkv_tiles) issue_tile(tile + 1, k1s, v1s);
-    step(k0s, v0s, tile);
-    wait_vmem();
-    __syncthreads();
-    if (it + 1 >= nkv_tiles) break;
-    if (it + 2 < nkv_tiles) issue_tile(tile + 2, k0s, v0s);
-    step(k1s, v1s, tile + 1);
-    wait_vmem();
-    __syncthreads();
+  for (int t0 = 0; t0 < nkv_tiles; t0 += STAGES) {
+#pragma unroll
+    for (int u = 0; u < STAGES; ++u) {
+      const int t = t0 + u;
+      if (t >= nkv_tiles) break;
+      // refill slot t % STAGES with K of tile t+STAGES and V of tile t+STAGES-1
+      dma_k(kv_next_k, u);
+      dma_v(kv_next_v, u);
+      if (u % 2 == 0) {
+        iteration(sA, sB, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES));
+      } else {
+        iteration(sB, sA, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES));
+      }
+      // scalars of the next iteration (their wait is folded into the barrier's)
+      kv_next_k = tile_kv0(t + 1 + STAGES);
+      kv_next_v = tile_kv0(t + STAGES);
+      kv_cur = tile_kv0(t + 1);
+      bits_cur = mbits ? mbits[t + 1 < nkv_tiles ? t + 1 : nkv_tiles - 1] : full;
+      // slot (t+2) % STAGES must have landed; younger loads may fly
+      wait_vm_lgkm<kInFlight>();
+      block_sync();
+    }
   }
 
   // ---- epilogue
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = l_run + other_half(l_run);
   if (task.nsplit == 1) {
     if (qrow < a.Nq) {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
@@ -307,16 +445,15 @@ void attn_fwd_kernel(AttnArgs a) {
         }
       }
       if (a.lse && hh == 0) {
-        const float m_use = (m_run == kNegInf) ? 0.f : m_run;
         a.lse[((int64_t)b * a.H + h) * a.Nq + qrow] =
-            l_tot > 0.f ? (m_use + __log2f(l_tot)) * 0.69314718055994530942f : kNegInf;
+            l_tot > 0.f ? (m_run + __log2f(l_tot)) * 0.69314718055994530942f : kNegInf;
       }
     }
   } else {
-    // Split-K partial state: m (log2 domain, raw), l, O unnormalised
+    // Split-K partial state: reference m (log2 domain), l, O unnormalised
     float* slot = a.ws + ti * (int64_t)C::kTQ * (kD + 2);
     if (hh == 0) {
-      slot[q_local] = m_run;
+      slot[q_local] = l_tot > 0.f ? m_run : kNegInf;
       slot[C::kTQ + q_local] = l_tot;
     }
     float* os = slot + 2 * C::kTQ + (int64_t)q_local * kD;
@@ -383,11 +520,16 @@ __global__ __launch_bounds__(256) void splitk_merge_kernel(AttnArgs a) {
   }
 }
 
+// Ring depth per KV tile: four slots for 32-key tiles, two for 64-key tiles
+// (64 KB of LDS per workgroup either way, so two workgroups share a CU).
+constexpr int stages_for(int tkv) { return tkv == 32 ? 4 : 2; }
+
 template <int NWAVES, int TKV>
 hipError_t launch_variant(const AttnArgs& a, hipStream_t s) {
   const int64_t slots = ((int64_t)a.ntasks + 7) / 8 * 8;
   if (slots == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_fwd_kernel<NWAVES, TKV>), dim3((unsigned)slots), dim3(64 * NWAVES), 0, s, a);
+  hipLaunchKernelGGL((attn_fwd_kernel<NWAVES, TKV, stages_for(TKV)>), dim3((unsigned)slots), dim3(64 * NWAVES), 0,
+                     s, a);
   return hipGetLastError();
 }
 

@@ -12,7 +12,8 @@ namespace bsa {
 namespace {
 
 std::vector<CatalogEntry> build_catalog() {
-  // id = ((tq index) * 2 + tkv index) * 4 + split index
+  // id = ((tq index) * 2 + tkv index) * 4 + split index; 32-key tiles use a
+  // four-slot K/V ring, 64-key tiles a two-slot ring (same LDS footprint)
   const int tqs[] = {64, 128, 256};
   const int tkvs[] = {32, 64};
   const int splits[] = {1, 2, 4, 8};
@@ -20,7 +21,7 @@ std::vector<CatalogEntry> build_catalog() {
   int id = 0;
   for (int tq : tqs)
     for (int tkv : tkvs)
-      for (int s : splits) out.push_back(CatalogEntry{id++, tq, tkv, s, 2, tq / 32});
+      for (int s : splits) out.push_back(CatalogEntry{id++, tq, tkv, s, tkv == 32 ? 4 : 2, tq / 32});
   return out;
 }
 
