@@ -41,6 +41,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -86,6 +87,25 @@ __device__ inline float other_half(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   // lanes 0-31 find the partner in r[1], lanes 32-63 in r[0]; the other entry is x itself
   return (threadIdx.x & 32) ? __uint_as_float(r[0]) : __uint_as_float(r[1]);
+}
+
+// In-place updates for the rare paths (rescale, masking).  The tied
+// operands pin each result to the register it came from; written as plain
+// C++ the compiler gives the updated values new registers and then copies
+// the whole accumulator on the common path where the update did not run.
+__device__ inline void scale_inplace(f32x16& v, float alpha) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    float x = v[i];
+    asm volatile("v_mul_f32_e32 %0, %1, %0" : "+v"(x) : "v"(alpha));
+    v[i] = x;
+  }
+}
+
+// x = keep ? x : -inf, in place (keep is per lane)
+__device__ inline void mask_inplace(float& x, bool keep) {
+  const float ninf = -__builtin_huge_valf();
+  asm volatile("v_cndmask_b32_e64 %0, %1, %0, %2" : "+v"(x) : "v"(ninf), "s"(__ballot(keep)));
 }
 
 // The running maximum is only raised when a tile's maximum exceeds it by more
@@ -144,7 +164,7 @@ void attn_fwd_kernel(AttnArgs a) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int w = tid >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int n = lane & 31;   // query row of this lane inside the wave
   const int hh = lane >> 5;  // lane half
   const int b = task.bh / a.H, h = task.bh - b * a.H;
@@ -175,12 +195,14 @@ void attn_fwd_kernel(AttnArgs a) {
   ci32p kvt = (ci32p)(a.kv_tile + tb);
   cu64p mbits = a.member ? (cu64p)(a.member + tb) : nullptr;
 
-  // ---- direct global -> LDS loads
+  // ---- K/V tiles: buffer loads straight into LDS
   // One instruction moves 64 lanes x 16 bytes = 4 token rows into 1 KB of
   // LDS, lane i landing at byte 16 * i.  Lane i of load j owns LDS row
-  // rr = 4 * (w + j * NWAVES) + i / 16 and physical chunk i % 16, and fetches
-  // the logical chunk that the swizzle places there.  Addresses are a
-  // wave-uniform tile base plus a per-lane 32-bit offset fixed for the task.
+  // rr = 4 * (w + j * NWAVES) + i / 16 and physical chunk i % 16, and reads
+  // the logical chunk that the swizzle places there, at a per-lane byte
+  // offset fixed for the whole task.  Each tile gets a buffer descriptor
+  // whose size covers only the tile's tokens inside the sequence, so rows
+  // past the end read as zero with no extra instruction.
   constexpr int kLoadsPerWave = TKV / (4 * NWAVES);
   static_assert(kLoadsPerWave >= 1 && TKV % (4 * NWAVES) == 0, "tile rows must split over the waves");
   const char* kbase = reinterpret_cast<const char*>(a.k + b * a.ks0 + h * a.ks1);
@@ -196,24 +218,13 @@ void attn_fwd_kernel(AttnArgs a) {
   }
   // copy the TKV tokens starting at kv0 into one ring slot
   auto dma_rows = [&](const char* base, int64_t stride, const uint32_t* offs, int kv0, uint8_t* dst_arr) {
-    const char* t0 = base + (int64_t)kv0 * stride;
-    if (kv0 + TKV <= a.Nkv) {
+    const int rows = min(TKV, a.Nkv - kv0);
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(base + (int64_t)kv0 * stride), 0, (int)(rows * stride), 0x00020000);
 #pragma unroll
-      for (int j = 0; j < kLoadsPerWave; ++j)
-        __builtin_amdgcn_global_load_lds(t0 + offs[j],
-                                         (__attribute__((address_space(3))) void*)(dst_arr + 1024 * (w + j * NWAVES)),
-                                         16, 0, 0);
-    } else {
-      // sequence tail: rows past the end read the zero page
-#pragma unroll
-      for (int j = 0; j < kLoadsPerWave; ++j) {
-        const int rr = 4 * (w + j * NWAVES) + (lane >> 4);
-        const void* p = (kv0 + rr < a.Nkv) ? static_cast<const void*>(t0 + offs[j])
-                                            : static_cast<const void*>(a.zero_page);
-        __builtin_amdgcn_global_load_lds(p, (__attribute__((address_space(3))) void*)(dst_arr + 1024 * (w + j * NWAVES)),
-                                         16, 0, 0);
-      }
-    }
+    for (int j = 0; j < kLoadsPerWave; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rsrc, (__attribute__((address_space(3))) void*)(dst_arr + 1024 * (w + j * NWAVES)), 16, offs[j], 0, 0, 0);
   };
   auto dma_k = [&](int kv0, int slot) { dma_rows(kbase, kstride, koffs, kv0, kslot(slot)); };
   auto dma_v = [&](int kv0, int slot) { dma_rows(vbase, vstride, voffs, kv0, vslot(slot)); };
@@ -245,6 +256,7 @@ void attn_fwd_kernel(AttnArgs a) {
   const int mem_bits = a.gq * a.gkv;
   const uint64_t full = (mem_bits >= 64) ? ~0ull : ((1ull << mem_bits) - 1);
   const float c_log2 = a.scale_log2;
+  const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
   f32x16 o[4];
 #pragma unroll
@@ -284,40 +296,40 @@ void attn_fwd_kernel(AttnArgs a) {
 
   // entries outside the tile's active members or past the sequence end -> -inf
   auto apply_mask = [&](f32x16* s, int kv0, uint64_t bits) {
-    if (__builtin_expect(kv0 + TKV > a.Nkv || bits != full, 0)) {
-      const uint64_t rowbits = bits >> (mem_row * a.gkv);
-      // allowed-key bitmap of this lane's row over the tile
-      uint64_t allowed = 0;
-      const int nvalid = min(TKV, a.Nkv - kv0);
-      const uint64_t tailmask = nvalid >= 64 ? ~0ull : ((1ull << nvalid) - 1);
-      if (a.gkv > 1) {
-        const int bkv = 1 << a.bkv_shift;
-        const uint64_t run = bkv >= 64 ? ~0ull : ((1ull << bkv) - 1);
-        for (int cm = 0; cm < a.gkv; ++cm)
-          if ((rowbits >> cm) & 1ull) allowed |= run << (cm * bkv);
-      } else {
-        allowed = (rowbits & 1ull) ? ~0ull : 0ull;
-      }
-      allowed &= tailmask;
-      const uint64_t mine = allowed >> (4 * hh);
+    const uint64_t rowbits = bits >> (mem_row * a.gkv);
+    // allowed-key bitmap of this lane's row over the tile
+    uint64_t allowed = 0;
+    const int nvalid = min(TKV, a.Nkv - kv0);
+    const uint64_t tailmask = nvalid >= 64 ? ~0ull : ((1ull << nvalid) - 1);
+    if (a.gkv > 1) {
+      const int bkv = 1 << a.bkv_shift;
+      const uint64_t run = bkv >= 64 ? ~0ull : ((1ull << bkv) - 1);
+      for (int cm = 0; cm < a.gkv; ++cm)
+        if ((rowbits >> cm) & 1ull) allowed |= run << (cm * bkv);
+    } else {
+      allowed = (rowbits & 1ull) ? ~0ull : 0ull;
+    }
+    allowed &= tailmask;
+    const uint64_t mine = allowed >> (4 * hh);
 #pragma unroll
-      for (int kb = 0; kb < kNKB; ++kb) {
+    for (int kb = 0; kb < kNKB; ++kb) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int jc = kb * 32 + (i >> 2) * 8 + (i & 3);  // key index minus 4 * hh
-          s[kb][i] = ((mine >> jc) & 1ull) ? s[kb][i] : kNegInf;
-        }
+      for (int i = 0; i < 16; ++i) {
+        const int jc = kb * 32 + (i >> 2) * 8 + (i & 3);  // key index minus 4 * hh
+        float x = s[kb][i];
+        mask_inplace(x, (mine >> jc) & 1ull);
+        s[kb][i] = x;
       }
     }
   };
 
-  // One pipeline iteration over tile t (scores in s_cur): mask, row max and
-  // the rare rescale; then the S^T MFMAs of the next tile (from ks_next)
-  // interleaved with the probabilities of this tile, and the O^T MFMAs of
-  // this tile (V from vs_cur) interleaved with the rest of them.
+  // One pipeline iteration over tile t (scores in s_cur): mask (rare), row
+  // max and the rare rescale; then the S^T MFMAs of the next tile (from
+  // ks_next) interleaved with the probabilities of this tile, and the O^T
+  // MFMAs of this tile (V from vs_cur) interleaved with the rest of them.
   auto iteration = [&](f32x16* s_cur, f32x16* s_nxt, int kv0_cur, uint64_t bits_cur, const uint8_t* ks_next,
                        const uint8_t* vs_cur) {
-    apply_mask(s_cur, kv0_cur, bits_cur);
+    if (__builtin_expect(kv0_cur + TKV > a.Nkv || bits_cur != full, 0)) apply_mask(s_cur, kv0_cur, bits_cur);
 
     // row maximum of the raw scores (the scale is positive)
     float mx = kNegInf;
@@ -336,19 +348,24 @@ void attn_fwd_kernel(AttnArgs a) {
       m_run = m_new;
       l_run *= alpha;
 #pragma unroll
-      for (int d = 0; d < 4; ++d) o[d] *= alpha;
+      for (int d = 0; d < 4; ++d) scale_inplace(o[d], alpha);
     }
     const float nm = (m_run == kNegInf) ? 0.f : -m_run;
 
 #pragma unroll
     for (int kb = 0; kb < kNKB; ++kb) s_nxt[kb] = f32x16{};
-    float ls[4] = {0.f, 0.f, 0.f, 0.f};
+    // row sums of the bf16 probabilities (the weights PV actually uses)
+    float ls0 = 0.f, ls1 = 0.f;
     bf16x8 pb[TKV / 16];
     // probability of element ei (chunk ei / 8, slot ei % 8 of that chunk)
     auto prob = [&](int ei) {
       const float p = fast_exp2(__builtin_fmaf(s_cur[ei / 16][ei % 16], c_log2, nm));
-      ls[ei & 3] += p;
       pb[ei / 8][ei % 8] = (__bf16)p;
+      if (ei & 1) {
+        const bf16x2 pair = {pb[ei / 8][(ei % 8) - 1], pb[ei / 8][ei % 8]};
+        if (ei & 2) ls1 = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, ls1, false);
+        else ls0 = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, ls0, false);
+      }
     };
     bf16x8 op[3];
     op[0] = load_op(0, ks_next, vs_cur);
@@ -369,7 +386,7 @@ void attn_fwd_kernel(AttnArgs a) {
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    l_run += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+    l_run += ls0 + ls1;
   };
 
   // number of DMA instructions one iteration issues (K tile and V tile)
@@ -412,16 +429,17 @@ void attn_fwd_kernel(AttnArgs a) {
       // refill slot t % STAGES with K of tile t+STAGES and V of tile t+STAGES-1
       dma_k(kv_next_k, u);
       dma_v(kv_next_v, u);
-      if (u % 2 == 0) {
-        iteration(sA, sB, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES));
-      } else {
-        iteration(sB, sA, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES));
-      }
-      // scalars of the next iteration (their wait is folded into the barrier's)
+      f32x16* s_cur = (u % 2 == 0) ? sA : sB;
+      f32x16* s_nxt = (u % 2 == 0) ? sB : sA;
+      iteration(s_cur, s_nxt, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES));
+      // scalars of the next iteration, complete before the barrier so no
+      // scalar load is outstanding while the next iteration's LDS reads are
+      // counted
       kv_next_k = tile_kv0(t + 1 + STAGES);
       kv_next_v = tile_kv0(t + STAGES);
       kv_cur = tile_kv0(t + 1);
       bits_cur = mbits ? mbits[t + 1 < nkv_tiles ? t + 1 : nkv_tiles - 1] : full;
+      asm volatile("" ::"s"(kv_next_k), "s"(kv_next_v), "s"(kv_cur), "s"(bits_cur));
       // slot (t+2) % STAGES must have landed; younger loads may fly
       wait_vm_lgkm<kInFlight>();
       block_sync();
