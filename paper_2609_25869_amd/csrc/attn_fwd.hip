@@ -323,23 +323,43 @@ void attn_fwd_kernel(AttnArgs a) {
     }
   };
 
-  // One pipeline iteration over tile t (scores in s_cur): mask (rare), row
-  // max and the rare rescale; then the S^T MFMAs of the next tile (from
-  // ks_next) interleaved with the probabilities of this tile, and the O^T
-  // MFMAs of this tile (V from vs_cur) interleaved with the rest of them.
-  auto iteration = [&](f32x16* s_cur, f32x16* s_nxt, int kv0_cur, uint64_t bits_cur, const uint8_t* ks_next,
-                       const uint8_t* vs_cur) {
-    if (__builtin_expect(kv0_cur + TKV > a.Nkv || bits_cur != full, 0)) apply_mask(s_cur, kv0_cur, bits_cur);
-
-    // row maximum of the raw scores (the scale is positive)
+  // Row maximum of one tile's raw scores (the scale is positive), both lane
+  // halves combined.
+  auto row_max = [&](const f32x16* s) -> float {
     float mx = kNegInf;
 #pragma unroll
     for (int kb = 0; kb < kNKB; ++kb) {
 #pragma unroll
-      for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(s_cur[kb][i], s_cur[kb][i + 1]));
+      for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(s[kb][i], s[kb][i + 1]));
     }
-    mx = fmaxf(mx, other_half(mx));
-    const float mxs = mx * c_log2;
+    return fmaxf(mx, other_half(mx));
+  };
+
+  // Distribution of the VALU work of one iteration over its MFMA units.
+  // Probabilities of all but the last 8-key chunk are formed during the
+  // S^T units (which have spare VALU slots); the last chunk during the first
+  // O^T units, before its MFMAs; the row maximum of the next tile's scores
+  // during the remaining O^T units, so the next iteration starts with it.
+  constexpr int kE = 16 * kNKB;         // score elements per lane
+  constexpr int kChunks = TKV / 16;     // 8-element P chunks
+  constexpr int kP = kE - 8;            // elements formed during the S^T units
+  constexpr int kJ1 = 4 * (kChunks - 1);  // first O^T unit that needs the last chunk
+  constexpr int kMx0 = 2;               // first O^T unit doing max steps
+  constexpr int kNmx = kE / 2;          // pairwise max steps
+  static_assert(kChunks >= 2, "pipeline needs two P chunks");
+
+  // One pipeline iteration over tile t: (rare) mask and max of s_cur, the
+  // reference update; then the S^T MFMAs of the next tile (from ks_next)
+  // interleaved with the probabilities of this tile, and the O^T MFMAs of
+  // this tile (V from vs_cur) interleaved with the rest of them and with the
+  // row maximum of the next tile.  Returns that maximum (raw scores).
+  auto iteration = [&](f32x16* s_cur, f32x16* s_nxt, float mx_cur, int kv0_cur, uint64_t bits_cur,
+                       const uint8_t* ks_next, const uint8_t* vs_cur) -> float {
+    if (__builtin_expect(kv0_cur + TKV > a.Nkv || bits_cur != full, 0)) {
+      apply_mask(s_cur, kv0_cur, bits_cur);
+      mx_cur = row_max(s_cur);
+    }
+    const float mxs = mx_cur * c_log2;
     // raise the reference only when needed (wave-uniform branch)
     const bool need = mxs > m_run + kTau;
     if (__ballot(need)) {
@@ -356,7 +376,8 @@ void attn_fwd_kernel(AttnArgs a) {
     for (int kb = 0; kb < kNKB; ++kb) s_nxt[kb] = f32x16{};
     // row sums of the bf16 probabilities (the weights PV actually uses)
     float ls0 = 0.f, ls1 = 0.f;
-    bf16x8 pb[TKV / 16];
+    float mxa = kNegInf, mxb = kNegInf;
+    bf16x8 pb[kChunks];
     // probability of element ei (chunk ei / 8, slot ei % 8 of that chunk)
     auto prob = [&](int ei) {
       const float p = fast_exp2(__builtin_fmaf(s_cur[ei / 16][ei % 16], c_log2, nm));
@@ -367,26 +388,41 @@ void attn_fwd_kernel(AttnArgs a) {
         else ls0 = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, ls0, false);
       }
     };
-    bf16x8 op[3];
-    op[0] = load_op(0, ks_next, vs_cur);
-    op[1] = load_op(1, ks_next, vs_cur);
+    // max step k covers elements 2k and 2k+1 of the next tile
+    auto max_step = [&](int k) {
+      const int e0 = 2 * k;
+      float& acc = (k & 1) ? mxb : mxa;
+      acc = fmaxf(acc, fmaxf(s_nxt[e0 / 16][e0 % 16], s_nxt[(e0 + 1) / 16][(e0 + 1) % 16]));
+    };
+    constexpr int kAhead = 3;  // operand read distance, in units
+    bf16x8 op[kAhead + 1];
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u) op[u] = load_op(u, ks_next, vs_cur);
 #pragma unroll
     for (int u = 0; u < kNU; ++u) {
-      if (u + 2 < kNU) op[(u + 2) % 3] = load_op(u + 2, ks_next, vs_cur);
+      if (u + kAhead < kNU) op[(u + kAhead) % (kAhead + 1)] = load_op(u + kAhead, ks_next, vs_cur);
       if (u < kNA) {
-        s_nxt[u % kNKB] = mfma32(op[u % 3], qf[u / kNKB], s_nxt[u % kNKB]);
-        prob(u);  // first half of the elements, one per unit
+        s_nxt[u % kNKB] = mfma32(op[u % (kAhead + 1)], qf[u / kNKB], s_nxt[u % kNKB]);
+#pragma unroll
+        for (int e = u * kP / kNA; e < (u + 1) * kP / kNA; ++e) prob(e);
       } else {
         const int j = u - kNA;
-        o[j % 4] = mfma32(op[u % 3], pb[j / 4], o[j % 4]);
-        if (j < kNB / 2) {  // second half, two per unit
-          prob(kNA + 2 * j);
-          prob(kNA + 2 * j + 1);
+        o[j % 4] = mfma32(op[u % (kAhead + 1)], pb[j / 4], o[j % 4]);
+        if (j < kJ1) {
+#pragma unroll
+          for (int e = kP + j * 8 / kJ1; e < kP + (j + 1) * 8 / kJ1; ++e) prob(e);
+        }
+        if (j >= kMx0) {
+          const int jj = j - kMx0, nj = kNB - kMx0;
+#pragma unroll
+          for (int k = jj * kNmx / nj; k < (jj + 1) * kNmx / nj; ++k) max_step(k);
         }
       }
       __builtin_amdgcn_sched_barrier(0);
     }
     l_run += ls0 + ls1;
+    const float mx_next = fmaxf(mxa, mxb);
+    return fmaxf(mx_next, other_half(mx_next));
   };
 
   // number of DMA instructions one iteration issues (K tile and V tile)
@@ -394,6 +430,7 @@ void attn_fwd_kernel(AttnArgs a) {
   constexpr int kInFlight = (STAGES - 2) * kGroup;
 
   f32x16 sA[kNKB], sB[kNKB];
+  float mx_cur = kNegInf;  // row maximum of the scores of the current tile
   // scalars for the coming iteration, fetched one iteration ahead
   int kv_next_k = 0, kv_next_v = 0, kv_cur = 0;
   uint64_t bits_cur = full;
@@ -417,6 +454,7 @@ void attn_fwd_kernel(AttnArgs a) {
     wait_vm_lgkm<(STAGES - 1) * kGroup>();
     block_sync();
     qk_only(kslot(0), sA);
+    mx_cur = row_max(sA);
     // the first iteration needs slot 1
     wait_vm_lgkm<kInFlight>();
     block_sync();  // every wave has read slot 0 before it is refilled
@@ -431,7 +469,7 @@ void attn_fwd_kernel(AttnArgs a) {
       dma_v(kv_next_v, u);
       f32x16* s_cur = (u % 2 == 0) ? sA : sB;
       f32x16* s_nxt = (u % 2 == 0) ? sB : sA;
-      iteration(s_cur, s_nxt, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES));
+      mx_cur = iteration(s_cur, s_nxt, mx_cur, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES));
       // scalars of the next iteration, complete before the barrier so no
       // scalar load is outstanding while the next iteration's LDS reads are
       // counted
