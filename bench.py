@@ -25,6 +25,11 @@ PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA, 256 CU x 4096 flop/clk x 2
 PEAK_HBM_GBS = 8000.0
 
 
+FLUSH_BYTES = 512 << 20
+KERNEL_SRC = os.path.join(HERE, "paper_2609_25869_amd", "csrc", "attn_fwd.hip")
+TRAFFIC_FILE = os.path.join(HERE, "profiles", "attn_fwd_c2_window15_traffic.md")
+
+
 def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
@@ -42,6 +47,37 @@ def effective_flops(mask, d):
             cols[-1] = mask.nkv - (m.shape[1] - 1) * bkv
             total += int(rows @ m.astype(np.int64) @ cols)
     return 4 * d * total
+
+
+def copy_probe(torch, mib):
+    """A plain device-to-device copy of known size, for scaling FETCH_SIZE / WRITE_SIZE."""
+    n = (mib << 20) // 4
+    src = torch.ones(n, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n * 4, "launches": 5}), flush=True)
+
+
+def measured_traffic(workload, plan_ids):
+    """HBM bytes per launch of the attention kernel from the committed counter summary.
+
+    Reported only when that summary was taken on this workload and plan with
+    the current kernel source; otherwise None.
+    """
+    import hashlib
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    text = open(TRAFFIC_FILE).read()
+    a = text.find("```json")
+    if a < 0:
+        return None
+    rec = json.loads(text[a + 7:text.index("```", a + 7)])
+    src_hash = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    if rec.get("workload") != workload or rec.get("plan_ids") != plan_ids or rec.get("attn_fwd_sha256") != src_hash:
+        return None
+    return rec["hbm_bytes_per_launch"]
 
 
 def cpu_baseline(q, k, v, mask, eff_flops_total, budget_s, seed=1234):
@@ -63,24 +99,25 @@ def cpu_baseline(q, k, v, mask, eff_flops_total, budget_s, seed=1234):
     def draw(n):
         return np.stack([rng.integers(0, B, n), rng.integers(0, H, n), rng.integers(0, Nq, n)], axis=1)
 
-    probe = draw(32)
-    t0 = time.perf_counter()
-    oattn.masked_attention(q, k, v, mask, rows=probe)
-    t_probe = time.perf_counter() - t0
-    per_row = max(t_probe / len(probe), 1e-6)
-    n = int(max(64, min(200000, budget_s / per_row)))
-    rows = draw(n)
-    t0 = time.perf_counter()
-    oattn.masked_attention(q, k, v, mask, rows=rows)
-    dt = time.perf_counter() - t0
-    f = row_flops(rows)
+    # batches of rows until the budget is spent (the first batch also warms the thread pool)
+    n, done, dt, f = 128, 0, 0.0, 0
+    while dt < budget_s:
+        rows = draw(n)
+        t0 = time.perf_counter()
+        oattn.masked_attention(q, k, v, mask, rows=rows)
+        t = time.perf_counter() - t0
+        dt += t
+        f += row_flops(rows)
+        done += n
+        if t < 2.0:
+            n *= 2
     return {
         "value": f / dt / 1e12,
         "unit": "TFLOP/s",
         "cores": oattn.num_threads(),
         "kind": "oracle",
         "sample": "%d seeded random query rows of the same workload (%.3g of %d rows, %.3g effective GFLOP), "
-                  "fp64 C oracle, %.1f s" % (n, n / (B * H * Nq), B * H * Nq, f / 1e9, dt),
+                  "fp64 C oracle, %.1f s" % (done, done / (B * H * Nq), B * H * Nq, f / 1e9, dt),
         "seconds": dt,
     }
 
@@ -88,12 +125,15 @@ def cpu_baseline(q, k, v, mask, eff_flops_total, budget_s, seed=1234):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c2_window15")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--force-plan", type=int, default=-1)
+    ap.add_argument("--no-flush", action="store_true", help="skip the cache-evicting write before each step")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB five times (HBM counter calibration) and exit")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -102,6 +142,9 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_probe:
+        copy_probe(torch, args.copy_probe)
+        return
     import paper_2609_25869_amd as bsa
     from workloads import CONFIGS, make_mask, make_qkv
 
@@ -124,9 +167,14 @@ def main():
     bq = [int(x) for x in mask.bq] if per_head else int(mask.bq[0])
     bkv = [int(x) for x in mask.bkv] if per_head else int(mask.bkv[0])
     stream = torch.cuda.current_stream()
+    # written before every step so that each request starts with the inputs
+    # out of the L2 and last-level caches (512 MiB is twice the MALL)
+    flush = None if args.no_flush else torch.empty(FLUSH_BYTES // 4, dtype=torch.int32, device=dev)
     torch.cuda.synchronize()
 
     def request():
+        if flush is not None:
+            flush.fill_(1)
         p = bsa.plan(md, bq, bkv, shapes, head_offset=list(mask.head_offset), stride_b=mask.stride_b,
                      force_plan=args.force_plan, stream=stream)
         e0 = torch.cuda.Event(enable_timing=True)
@@ -171,6 +219,7 @@ def main():
     kernel_tflops = eff / (k_avg * 1e-3) / 1e12
     executed = sum(4 * d * i["n_tiles"] * i["tq"] * i["tkv"] for i in info)   # MFMA work incl. masked entries
     tiles_bytes = sum(4 * d * i["n_tiles"] * i["tkv"] for i in info)   # K/V bytes streamed, bf16
+    traffic = measured_traffic(cfg.name, [i["plan_id"] for i in info])
     out = {
         "metric": "effective active-block TFLOP/s + request latency incl. planning, 1x MI355X",
         "value": eff / (ms_per_step * 1e-3) / 1e12,
@@ -194,8 +243,10 @@ def main():
             "parallelism": "single GPU",
         },
         "request_ms": {"median": float(np.median(req_ms)), "p95": float(np.percentile(req_ms, 95)),
+                       "cache_flush_before_each_step": flush is not None,
                        "warm_median": float(np.median(warm))},
-        "kernel_ms": {"mean": k_avg, "median": float(np.median(kernel_ms))},
+        "kernel_ms": {"mean": k_avg, "median": float(np.median(kernel_ms)),
+                      "p95": float(np.percentile(kernel_ms, 95))},
         "kernel_tflops": kernel_tflops,
         "executed_kernel_tflops": executed / (k_avg * 1e-3) / 1e12,
         "plans": [{k2: i[k2] for k2 in ("plan_id", "tq", "tkv", "split", "mapping_name", "regime_hit", "n_tasks",
@@ -207,7 +258,7 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": kernel_tflops / PEAK_BF16_TFLOPS,
-            "traffic": None,
+            "traffic": traffic,
             "kv_stream_gbs": tiles_bytes / (k_avg * 1e-3) / 1e9,
         },
     }

@@ -44,6 +44,9 @@
 extern "C" {
 #endif
 
+/* Only the entry points below are exported from the shared library. */
+#define BSA_API __attribute__((visibility("default")))
+
 #define BSA_VERSION_MAJOR 1
 #define BSA_VERSION_MINOR 0
 #define BSA_MAX_SEGMENTS 16
@@ -138,48 +141,48 @@ enum {
 };
 
 /* Library version. */
-bsa_status bsa_version(int32_t* major, int32_t* minor);
+BSA_API bsa_status bsa_version(int32_t* major, int32_t* minor);
 
 /* Human-readable name of a status code (static storage). */
-const char* bsa_status_string(bsa_status s);
+BSA_API const char* bsa_status_string(bsa_status s);
 
 /* Detail of the last failure on the calling thread (thread-local storage,
  * valid until the next call on this thread). */
-const char* bsa_last_error(void);
+BSA_API const char* bsa_last_error(void);
 
 /* Load a plan-table artifact (Section 5.1: catalog + plan table + feature
  * schema, versioned together).  Host only.  Fails with BSA_ERR_LUT when the
  * file is missing or malformed, or its architecture, format version or
  * catalog does not match this library.  *out is NULL on failure. */
-bsa_status bsa_lut_load(const char* path, bsa_lut_t* out);
-bsa_status bsa_lut_destroy(bsa_lut_t lut);
+BSA_API bsa_status bsa_lut_load(const char* path, bsa_lut_t* out);
+BSA_API bsa_status bsa_lut_destroy(bsa_lut_t lut);
 
 /* The ranking Pi_A(r) for regime query z (Eq. 4), written to plans[0..cap).
  * *n receives the ranking length, *hit 1 if the table holds the regime and 0
  * if the lookup missed (then the ranking is the key's base plan alone,
  * Algorithm 2).  Host only; lut NULL means the default table. */
-bsa_status bsa_lut_rank(bsa_lut_t lut, const bsa_regime_query* z, int32_t* plans, int32_t cap,
+BSA_API bsa_status bsa_lut_rank(bsa_lut_t lut, const bsa_regime_query* z, int32_t* plans, int32_t cap,
                         int32_t* n, int32_t* hit);
 
 /* Algorithm 2 on given statistics: the first eligible plan of the ranking for
  * z, for tensors of shape `shapes`.  BSA_ERR_UNSUPPORTED (and *plan_id = -1)
  * when none is eligible.  Host only. */
-bsa_status bsa_select_plan(bsa_lut_t lut, const bsa_regime_query* z, const bsa_shapes* shapes,
+BSA_API bsa_status bsa_select_plan(bsa_lut_t lut, const bsa_regime_query* z, const bsa_shapes* shapes,
                            int32_t* plan_id);
 
 /* Catalog introspection (Section 4.4).  Host only. */
-int32_t bsa_catalog_size(void);
-bsa_status bsa_catalog_get(int32_t id, bsa_catalog_entry* out);
+BSA_API int32_t bsa_catalog_size(void);
+BSA_API bsa_status bsa_catalog_get(int32_t id, bsa_catalog_entry* out);
 
 /* Eligible(P, R) of Section 4.4 for catalog plan `plan_id`, logical geometry
  * (bq, bkv) and shapes: supported dtype, head dim, layout, tile/block nesting
  * and membership size.  *eligible receives 0 or 1.  Host only. */
-bsa_status bsa_plan_eligible(int32_t plan_id, int32_t bq, int32_t bkv, const bsa_shapes* shapes,
+BSA_API bsa_status bsa_plan_eligible(int32_t plan_id, int32_t bq, int32_t bkv, const bsa_shapes* shapes,
                              int32_t* eligible);
 
 /* The base plan of request key (bq, bkv) (Section 5.1): a catalog plan
  * eligible for every request with that key.  Host only. */
-bsa_status bsa_base_plan(int32_t bq, int32_t bkv, int32_t* plan_id);
+BSA_API bsa_status bsa_base_plan(int32_t bq, int32_t bkv, int32_t* plan_id);
 
 /*
  * Plan a request.  B_Q/B_KV hold n_geom logical geometries: n_geom == 1 for
@@ -189,7 +192,7 @@ bsa_status bsa_base_plan(int32_t bq, int32_t bkv, int32_t* plan_id);
  * the statistics copy.  On success *out owns the plan; on failure *out is
  * NULL and nothing is leaked.
  */
-bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_KV, int32_t n_geom,
+BSA_API bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_KV, int32_t n_geom,
                     const bsa_shapes* shapes, const bsa_plan_opts* opts, void* stream,
                     bsa_plan_t* out);
 
@@ -201,24 +204,24 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
  * synchronising call.  Calls on one plan must not overlap in time (the
  * Split-K workspace is shared).
  */
-bsa_status bsa_forward(bsa_plan_t plan, const void* q, const void* k, const void* v, void* o, float* lse,
+BSA_API bsa_status bsa_forward(bsa_plan_t plan, const void* q, const void* k, const void* v, void* o, float* lse,
                        void* stream);
 
 /* Number of geometry segments of a plan and the summary of one. */
-bsa_status bsa_plan_num_segments(bsa_plan_t plan, int32_t* n);
-bsa_status bsa_plan_info(bsa_plan_t plan, int32_t segment, bsa_segment_info* out);
+BSA_API bsa_status bsa_plan_num_segments(bsa_plan_t plan, int32_t* n);
+BSA_API bsa_status bsa_plan_info(bsa_plan_t plan, int32_t segment, bsa_segment_info* out);
 
 /* Heads of a segment, ascending, into heads[0..cap); *n receives the count. */
-bsa_status bsa_plan_segment_heads(bsa_plan_t plan, int32_t segment, int32_t* heads, int32_t cap, int32_t* n);
+BSA_API bsa_status bsa_plan_segment_heads(bsa_plan_t plan, int32_t segment, int32_t* heads, int32_t cap, int32_t* n);
 
 /* Copy plan metadata to host memory (synchronises the plan's stream).
  * `segment` is ignored for the logical mask-state exports.  *needed receives
  * the size in bytes; with host_buf NULL nothing is copied. */
-bsa_status bsa_plan_export(bsa_plan_t plan, int32_t segment, int32_t what, void* host_buf, size_t bytes,
+BSA_API bsa_status bsa_plan_export(bsa_plan_t plan, int32_t segment, int32_t what, void* host_buf, size_t bytes,
                            size_t* needed);
 
 /* Release a plan (stream-ordered on the plan's stream). */
-bsa_status bsa_plan_destroy(bsa_plan_t plan);
+BSA_API bsa_status bsa_plan_destroy(bsa_plan_t plan);
 
 #ifdef __cplusplus
 }

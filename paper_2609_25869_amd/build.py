@@ -32,7 +32,9 @@ def common_flags():
     return ["-O3", "-std=c++17", "-fPIC", "--offload-arch=%s" % ARCH,
             # keep packed-fp32 instructions out of the generated code
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-I", os.path.join(ROOT, "include"), "-Wall", "-Wno-unused-result"]
+            "-I", os.path.join(ROOT, "include"), "-Wall", "-Wno-unused-result",
+            # export only the C-ABI (declared BSA_API in bsa.h)
+            "-fvisibility=hidden"]
 
 
 # Per-file flags.  The attention kernel never produces NaN from finite
