@@ -31,6 +31,12 @@ struct SegStats {
   unsigned long long nnz, run_blocks, max_row_nnz, pad;
 };
 
+// A range of logical rows inside one (b, h), reduced by one workgroup.
+struct RowChunk {
+  int64_t begin, end;
+  int32_t bh, seg;
+};
+
 struct MaskStateArgs {
   const uint8_t* mask;
   int64_t stride_b;
@@ -39,6 +45,9 @@ struct MaskStateArgs {
   int32_t H, nbh;
   int64_t R;
   int32_t* counts;          // [R]   (count pass)
+  int32_t* runs;            // [R]   (count pass) active blocks of the row in runs of length >= 2
+  const RowChunk* chunks;   // [nchunks] (count pass) reduction ranges
+  int32_t nchunks;
   const int64_t* row_ptr;   // [R+1] (fill pass)
   int32_t* col_idx;         // [nnz] (fill pass)
   SegStats* seg_stats;      // [nseg]

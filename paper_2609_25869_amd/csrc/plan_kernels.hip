@@ -56,11 +56,49 @@ __global__ __launch_bounds__(256) void mask_rows_kernel(MaskStateArgs a) {
   }
   if (!kFill && lane == 0) {
     a.counts[r] = (int32_t)nnz;
-    SegStats* st = a.seg_stats + hd.seg;
-    atomicAdd(&st->nnz, (unsigned long long)nnz);
-    atomicAdd(&st->run_blocks, (unsigned long long)run);
-    atomicMax(&st->max_row_nnz, (unsigned long long)nnz);
-    atomicAdd(a.bh_nnz + bh, (unsigned long long)nnz);
+    a.runs[r] = (int32_t)run;
+  }
+}
+
+// Statistics of mu(M) from the per-row counts: one workgroup per row chunk
+// (a chunk never crosses a (b, h) boundary), so only a handful of atomics
+// per chunk reach the shared per-segment counters.
+constexpr int kStatThreads = 256;
+
+__global__ __launch_bounds__(kStatThreads) void row_stats_kernel(MaskStateArgs a) {
+  const RowChunk ch = a.chunks[blockIdx.x];
+  unsigned long long nnz = 0, run = 0, mx = 0;
+  for (int64_t r = ch.begin + threadIdx.x; r < ch.end; r += kStatThreads) {
+    const unsigned long long c = (unsigned long long)a.counts[r];
+    nnz += c;
+    run += (unsigned long long)a.runs[r];
+    mx = c > mx ? c : mx;
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    nnz += __shfl_xor(nnz, off, 64);
+    run += __shfl_xor(run, off, 64);
+    const unsigned long long o = __shfl_xor(mx, off, 64);
+    mx = o > mx ? o : mx;
+  }
+  __shared__ unsigned long long part[3][kStatThreads / 64];
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    part[0][w] = nnz;
+    part[1][w] = run;
+    part[2][w] = mx;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 1; i < kStatThreads / 64; ++i) {
+      nnz += part[0][i];
+      run += part[1][i];
+      mx = part[2][i] > mx ? part[2][i] : mx;
+    }
+    SegStats* st = a.seg_stats + ch.seg;
+    atomicAdd(&st->nnz, nnz);
+    atomicAdd(&st->run_blocks, run);
+    atomicMax(&st->max_row_nnz, mx);
+    atomicAdd(a.bh_nnz + ch.bh, nnz);
   }
 }
 
@@ -247,6 +285,7 @@ inline unsigned grid_for(int64_t rows, int per_block) { return (unsigned)((rows 
 hipError_t launch_mask_count(const MaskStateArgs& a, hipStream_t s) {
   if (a.R == 0) return hipSuccess;
   hipLaunchKernelGGL(mask_rows_kernel<false>, dim3(grid_for(a.R, kRowsPerBlock)), dim3(256), 0, s, a);
+  if (a.nchunks > 0) hipLaunchKernelGGL(row_stats_kernel, dim3((unsigned)a.nchunks), dim3(kStatThreads), 0, s, a);
   return hipGetLastError();
 }
 

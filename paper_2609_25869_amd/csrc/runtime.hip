@@ -486,6 +486,15 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
   }
   const int nseg = (int)p->segs.size();
 
+  // row chunks for the statistics reduction: within one (b, h), at most 2048 rows each
+  std::vector<RowChunk> chunks;
+  for (int b = 0; b < B; ++b)
+    for (int h = 0; h < H; ++h) {
+      const int bh = b * H + h;
+      for (int64_t r = p->row_base[bh]; r < p->row_base[bh + 1]; r += 2048)
+        chunks.push_back(RowChunk{r, std::min<int64_t>(r + 2048, p->row_base[bh + 1]), bh, p->heads[h].seg});
+    }
+
   // ---- device buffer before the statistics synchronisation
   const size_t o_zero = 0;
   const size_t o_heads = align256(o_zero + 256);
@@ -493,9 +502,11 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
   const size_t o_sheads = align256(o_rbase + sizeof(int64_t) * p->row_base.size());
   const size_t o_stats = align256(o_sheads + sizeof(int32_t) * seg_heads.size());
   const size_t o_bhnnz = align256(o_stats + sizeof(SegStats) * nseg);
-  const size_t upload_bytes = o_bhnnz + sizeof(unsigned long long) * (size_t)B * H;
+  const size_t o_chunks = align256(o_bhnnz + sizeof(unsigned long long) * (size_t)B * H);
+  const size_t upload_bytes = o_chunks + sizeof(RowChunk) * chunks.size();
   const size_t o_counts = align256(upload_bytes);
-  const size_t o_rowptr = align256(o_counts + sizeof(int32_t) * (size_t)p->R);
+  const size_t o_runs = align256(o_counts + sizeof(int32_t) * (size_t)p->R);
+  const size_t o_rowptr = align256(o_runs + sizeof(int32_t) * (size_t)p->R);
   const size_t o_scan = align256(o_rowptr + sizeof(int64_t) * (size_t)(p->R + 1));
   const size_t pre_bytes = o_scan + sizeof(int64_t) * (size_t)scan_tmp_elems(p->R);
   void* pre = nullptr;
@@ -522,6 +533,7 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
     std::memcpy(h8 + o_heads, p->heads.data(), sizeof(HeadDesc) * H);
     std::memcpy(h8 + o_rbase, p->row_base.data(), sizeof(int64_t) * p->row_base.size());
     std::memcpy(h8 + o_sheads, seg_heads.data(), sizeof(int32_t) * seg_heads.size());
+    if (!chunks.empty()) std::memcpy(h8 + o_chunks, chunks.data(), sizeof(RowChunk) * chunks.size());
     HIP_TRY(hipMemcpyAsync(pre8, h8, upload_bytes, hipMemcpyHostToDevice, stream));
 
     // mu(M): row counts and statistics, then the block-CSR offsets
@@ -534,6 +546,9 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
     ma.nbh = B * H;
     ma.R = p->R;
     ma.counts = p->counts_dev;
+    ma.runs = reinterpret_cast<int32_t*>(pre8 + o_runs);
+    ma.chunks = reinterpret_cast<const RowChunk*>(pre8 + o_chunks);
+    ma.nchunks = (int32_t)chunks.size();
     ma.seg_stats = p->stats_dev;
     ma.bh_nnz = p->bh_nnz_dev;
     HIP_TRY(launch_mask_count(ma, stream));
