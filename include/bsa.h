@@ -19,7 +19,7 @@
  *               metadata on the GPU (physical tiles, membership, tasks,
  *               Split-K workspace; Section 4);
  *   bsa_forward runs the plan's kernels on any Q/K/V/O of the planned shapes
- *               (warm repeats reuse the prepared plan; Section 6.4).
+ *               (warm repeats reuse the prepared plan; Section 7.4).
  *
  * Conventions
  *   - Every entry point returns a bsa_status and never throws.  On failure a

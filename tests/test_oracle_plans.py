@@ -156,7 +156,7 @@ def test_split_chunks_partition_rows():
 
 def test_intensity_accounting_table4():
     """Q-resident accounting: per tile 4*d*T_Q*T_KV flop over 4*d*T_KV K/V bytes -> T_Q flop/byte
-    (Section 2.3; Table 4 lists intensity = B_Q for Direct tiles)."""
+    (Section 2.3; Table 3 lists intensity = B_Q for Direct tiles)."""
     table4 = {(128, 128): 128.0, (128, 64): 128.0, (64, 64): 64.0, (64, 32): 64.0,
               (32, 32): 32.0, (32, 16): 32.0, (16, 16): 16.0}
     d = 128

@@ -2,7 +2,7 @@
 
 Inputs follow the shapes of the paper's vDiT workloads (about 115K tokens for
 a five-second 720p clip, Section 1; logical blocks of 16 to 128 tokens and
-mean densities near 10%, Section 6.1 and Table 4).  The paper's real mask
+mean densities near 10%, Section 7.1 and Table 3).  The paper's real mask
 corpus is not available, so these generators stand in for it:
 
 * Q, K, V: i.i.d. N(0, 1) in float32 rounded to bfloat16, drawn per
