@@ -581,6 +581,7 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
     if (sg.tiles_bound >= INT32_MAX || sg.Rp >= INT32_MAX)
       return fail(BSA_ERR_UNSUPPORTED, "too many active tiles for 32-bit tile indices");
     sg.tasks_bound = e.split == 1 ? sg.Rp : std::min(sg.Rp * e.split, sg.Rp + sg.tiles_bound);
+    if (sg.tasks_bound >= INT32_MAX) return fail(BSA_ERR_UNSUPPORTED, "too many tasks for one launch");
   }
   if (p->nnz >= INT32_MAX) return fail(BSA_ERR_UNSUPPORTED, "too many active blocks");
 

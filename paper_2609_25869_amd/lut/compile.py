@@ -1,0 +1,172 @@
+"""Plan-table compilation (Section 5.1, Algorithm 1, regimes-and-rankings part).
+
+Input: the JSON lines written by ``profile.py`` (one per profiling case: the
+request key, the regime features and the validated median latency of every
+plan).  Output: the ``bsa-plan-table`` artifact that ``bsa_lut_load`` reads.
+
+Rules:
+* cases are grouped by request key (B_Q, B_KV, dtype, head dim);
+* within a key, each case falls in the bucket given by the feature schema:
+  for every feature, the number of bucket edges <= its value; density
+  (active / all logical blocks) and run coverage (active blocks in runs of
+  length >= 2 / active blocks) are compared exactly as integers,
+  num * 10000 >= edge * den;
+* in every bucket the plans with a valid latency on *every* case of the
+  bucket are ranked by increasing geometric-mean latency over the bucket,
+  exact ties by plan id, and the key's base plan is appended.
+
+    python -m paper_2609_25869_amd.lut.compile --profile P.jsonl [--eval E.jsonl] --out gfx950_v1.json
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+from typing import Dict, List, Sequence, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+# Feature schema of the first gfx950 table: predefined bucket edges.
+# seq_q in tokens, batch_heads in (batch x heads), ratios in units of 1e-4.
+SCHEMA: List[Tuple[str, List[int]]] = [
+    ("seq_q", [32768, 98304]),
+    ("batch_heads", [12]),
+    ("density", [700, 2000]),
+    ("run_coverage", [5000]),
+]
+
+
+def load_records(path: str) -> List[Dict]:
+    with open(path) as f:
+        return [json.loads(line) for line in f if line.strip()]
+
+
+def feature_value(feats: Dict, name: str):
+    if name == "density":
+        return feats["nnz"], feats["blocks"]
+    if name == "run_coverage":
+        return feats["run_blocks"], feats["nnz"]
+    return feats[name]
+
+
+def bucket(feats: Dict, schema: Sequence[Tuple[str, Sequence[int]]]) -> Tuple[int, ...]:
+    out = []
+    for name, edges in schema:
+        v = feature_value(feats, name)
+        if isinstance(v, tuple):
+            num, den = v
+            if den <= 0:
+                num, den = 0, 1
+            out.append(sum(1 for e in edges if num * 10000 >= e * den))
+        else:
+            out.append(sum(1 for e in edges if v >= e))
+    return tuple(out)
+
+
+def compile_table(records: Sequence[Dict], schema, base_plan) -> Dict[Tuple[int, ...], Dict[Tuple[int, ...], List[int]]]:
+    """{key: {bucket: ranking}} from profiling records."""
+    groups: Dict[Tuple[int, ...], Dict[Tuple[int, ...], List[Dict]]] = {}
+    for r in records:
+        key = tuple(r["key"])
+        groups.setdefault(key, {}).setdefault(bucket(r["features"], schema), []).append(r)
+    table = {}
+    for key, buckets in groups.items():
+        base = base_plan(key)
+        for b, cases in buckets.items():
+            common = None
+            for c in cases:
+                valid = {int(p) for p in c["latency_ms"]}
+                common = valid if common is None else common & valid
+            if not common:
+                continue
+
+            def geo_mean(p):
+                return math.exp(sum(math.log(c["latency_ms"][str(p)]) for c in cases) / len(cases))
+
+            ranking = sorted(common, key=lambda p: (geo_mean(p), p))
+            table.setdefault(key, {})[b] = ranking + [base]
+    return table
+
+
+def artifact(table, schema, catalog, provenance: Dict) -> Dict:
+    regimes = []
+    for key in sorted(table):
+        for b in sorted(table[key]):
+            regimes.append({"key": list(key), "bucket": list(b), "ranking": table[key][b]})
+    return {
+        "format": "bsa-plan-table",
+        "version": 1,
+        "arch": "gfx950",
+        "catalog": [[e["id"], e["tq"], e["tkv"], e["split"], e["stages"], e["waves"]] for e in catalog],
+        "schema": [[n, list(e)] for n, e in schema],
+        "regimes": regimes,
+        "provenance": provenance,
+    }
+
+
+def select(table, schema, base_plan, key, feats) -> int:
+    """First plan of the ranking (every catalog plan is eligible for the corpus requests)."""
+    ranking = table.get(tuple(key), {}).get(bucket(feats, schema))
+    return ranking[0] if ranking else base_plan(tuple(key))
+
+
+def regret_report(table, schema, base_plan, records) -> Dict:
+    """Selected / fastest measured latency per case (1 is optimal)."""
+    regrets, misses, per_key = [], 0, {}
+    for r in records:
+        lat = {int(p): t for p, t in r["latency_ms"].items()}
+        if not lat:
+            continue
+        sel = select(table, schema, base_plan, r["key"], r["features"])
+        if tuple(r["key"]) not in table or bucket(r["features"], schema) not in table[tuple(r["key"])]:
+            misses += 1
+        best = min(lat.values())
+        g = lat.get(sel, float("nan")) / best
+        regrets.append(g)
+        per_key.setdefault("%d:%d" % tuple(r["key"][:2]), []).append(g)
+    regrets = [g for g in regrets if g == g]
+
+    def summary(xs):
+        xs = sorted(xs)
+        if not xs:
+            return {}
+        pct = lambda q: xs[min(len(xs) - 1, int(math.ceil(q * len(xs))) - 1)]
+        return {"cases": len(xs), "gm": math.exp(sum(math.log(x) for x in xs) / len(xs)), "p95": pct(0.95),
+                "p99": pct(0.99), "max": xs[-1], "within_3pct": sum(1 for x in xs if x <= 1.03) / len(xs)}
+
+    return {"all": summary(regrets), "lookup_misses": misses,
+            "per_key": {k: summary(v) for k, v in sorted(per_key.items())}}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--profile", default=os.path.join(HERE, "gfx950_profile.jsonl"))
+    ap.add_argument("--eval", default=os.path.join(HERE, "gfx950_eval.jsonl"))
+    ap.add_argument("--out", default=os.path.join(HERE, "gfx950_v1.json"))
+    args = ap.parse_args()
+    import paper_2609_25869_amd as bsa
+
+    base = lambda key: bsa.base_plan(key[0], key[1])
+    recs = load_records(args.profile)
+    table = compile_table(recs, SCHEMA, base)
+    prov = {"profiled_on": "MI355X (gfx950)", "profile_cases": len(recs),
+            "corpus": "seeded synthetic masks (frame windows, Bernoulli + diagonal, pooled q.k top-k), "
+                      "nine paper geometries + (128,32)/(32,128), N in {16K, 64K, 115K}, 4 or 24 batch x heads",
+            "latency": "median of 3 kernel runs after 1 warm-up, HIP events"}
+    if os.path.exists(args.eval):
+        ev = load_records(args.eval)
+        prov["eval_cases"] = len(ev)
+        prov["eval_regret"] = regret_report(table, SCHEMA, base, ev)["all"]
+    prov["profile_regret"] = regret_report(table, SCHEMA, base, recs)["all"]
+    doc = artifact(table, SCHEMA, bsa.catalog(), prov)
+    with open(args.out, "w") as f:
+        json.dump(doc, f, indent=1)
+        f.write("\n")
+    print(json.dumps(prov, indent=1))
+    if os.path.exists(args.eval):
+        print(json.dumps(regret_report(table, SCHEMA, base, load_records(args.eval)), indent=1))
+
+
+if __name__ == "__main__":
+    main()

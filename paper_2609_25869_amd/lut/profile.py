@@ -1,0 +1,195 @@
+"""Offline profiling of the plan catalog on MI355X (Section 5.1, Algorithm 1).
+
+Runs every eligible catalog plan on a corpus of seeded synthetic masks and
+records, per case, the request key, the regime features the online path will
+see (the library's own mask statistics) and the median kernel latency of each
+plan whose output passed validation.  The output is one JSON line per case;
+``compile.py`` turns those lines into the plan table.
+
+Validation: every plan's output must be finite and agree with the key's base
+plan within 2e-2 absolute (each plan is independently parity-tested against
+the fp64 definition; here the check only guards the profiling run itself).
+
+Corpus (the paper's profiling masks are not available; these stand in):
+  geometries: the nine logical geometries of the paper's workloads plus the
+  alternating (128,32) / (32,128) pair; sequence lengths 16K, 64K and 115K
+  tokens; 4 or 24 (batch x heads); masks from three families at several
+  densities -- frame-window masks (long runs, like spatiotemporal windows),
+  Bernoulli masks with the diagonal (few runs) and per-row top-k of pooled
+  q.k block scores with the diagonal.  Inputs are N(0,1) in bf16.
+
+    python -m paper_2609_25869_amd.lut.profile --out PATH [--split profile|eval] [--budget SECONDS]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+GEOMETRIES = [(128, 128), (128, 64), (64, 64), (64, 32), (32, 32), (32, 16), (16, 16), (128, 32), (32, 128)]
+SEQ_LENS = [16384, 65536, 115200]
+BATCH_HEADS = [4, 24]
+FAMILIES = [("window", 0.05), ("window", 0.15), ("bernoulli", 0.03), ("bernoulli", 0.10), ("bernoulli", 0.30),
+            ("topk", 0.12)]
+SPLIT_SEED = {"profile": 0, "eval": 1}
+FRAMES = 16
+
+
+def log(msg):
+    print("[profile] " + msg, flush=True)
+
+
+def corpus(split):
+    """The deterministic case list of one split."""
+    cases = []
+    for gi, geom in enumerate(GEOMETRIES):
+        for N in SEQ_LENS:
+            for bh in BATCH_HEADS:
+                for fi, (fam, rho) in enumerate(FAMILIES):
+                    seed = ((SPLIT_SEED[split] * 16 + gi) * 8 + SEQ_LENS.index(N)) * 64 + BATCH_HEADS.index(bh) * 8 + fi
+                    cases.append(dict(id="%s-%d" % (split, len(cases)), geometry=list(geom), N=N, bh=bh, family=fam,
+                                      rho=rho, seed=seed))
+    return cases
+
+
+def make_mask(torch, case, q, k):
+    """[bh, nqb, nkb] uint8 mask for the case, built on the device."""
+    bq, bkv = case["geometry"]
+    N, bh, rho = case["N"], case["bh"], case["rho"]
+    nqb, nkb = -(-N // bq), -(-N // bkv)
+    dev = q.device
+    g = torch.Generator(device=dev)
+    g.manual_seed(case["seed"])
+    cq = (torch.arange(nqb, device=dev, dtype=torch.float64) + 0.5) * bq
+    ck = (torch.arange(nkb, device=dev, dtype=torch.float64) + 0.5) * bkv
+    diag = (torch.arange(nqb, device=dev)[:, None] * bq < (torch.arange(nkb, device=dev)[None, :] + 1) * bkv) & \
+           (torch.arange(nkb, device=dev)[None, :] * bkv < (torch.arange(nqb, device=dev)[:, None] + 1) * bq)
+    out = torch.empty((bh, nqb, nkb), dtype=torch.uint8, device=dev)
+    if case["family"] == "window":
+        # tokens as FRAMES frames of N/FRAMES positions; active when the block
+        # centres are within one frame and within a spatial half-width w
+        F = N / FRAMES
+        fq, fk = torch.floor(cq / F), torch.floor(ck / F)
+        sq, sk = cq - fq * F, ck - fk * F
+        w = rho * FRAMES / 3.0 * F / 2.0
+        for h in range(bh):
+            jitter = float(torch.rand(1, generator=g, device=dev).item()) * 0.2 + 0.9
+            m = ((fq[:, None] - fk[None, :]).abs() <= 1) & ((sq[:, None] - sk[None, :]).abs() <= w * jitter)
+            out[h] = (m | diag).to(torch.uint8)
+    elif case["family"] == "bernoulli":
+        for h in range(bh):
+            m = torch.rand((nqb, nkb), generator=g, device=dev) < rho
+            out[h] = (m | diag).to(torch.uint8)
+    else:
+        kk = max(1, int(math.floor(rho * nkb + 0.5)))
+        for h in range(bh):
+            pq = q[0, :nqb * bq, h, :].float().reshape(nqb, bq, -1).mean(1) if N % bq == 0 else \
+                torch.stack([q[0, i * bq:min(N, (i + 1) * bq), h, :].float().mean(0) for i in range(nqb)])
+            pk = k[0, :nkb * bkv, h, :].float().reshape(nkb, bkv, -1).mean(1) if N % bkv == 0 else \
+                torch.stack([k[0, i * bkv:min(N, (i + 1) * bkv), h, :].float().mean(0) for i in range(nkb)])
+            idx = torch.topk(pq @ pk.T, kk, dim=1).indices
+            m = torch.zeros((nqb, nkb), dtype=torch.bool, device=dev)
+            m.scatter_(1, idx, True)
+            out[h] = (m | diag).to(torch.uint8)
+    return out
+
+
+def profile_case(torch, bsa, case, reps=3):
+    bq, bkv = case["geometry"]
+    N, bh = case["N"], case["bh"]
+    dev = torch.device("cuda")
+    g = torch.Generator(device=dev)
+    g.manual_seed(case["seed"] + 7)
+    q = torch.randn((1, N, bh, 128), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    k = torch.randn((1, N, bh, 128), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    v = torch.randn((1, N, bh, 128), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    mask = make_mask(torch, case, q, k)
+    nqb, nkb = mask.shape[1], mask.shape[2]
+    head_offset = [h * nqb * nkb for h in range(bh)]
+    shapes = bsa.shapes_of(q, k, v, q)
+    o = torch.empty_like(q)
+    stream = torch.cuda.current_stream()
+    base = bsa.base_plan(bq, bkv)
+    plans = [e["id"] for e in bsa.catalog() if bsa.plan_eligible(e["id"], bq, bkv, shapes)]
+    plans = [base] + [p for p in plans if p != base]
+    ref = None
+    lat, invalid, feats = {}, [], None
+    for pid in plans:
+        try:
+            p = bsa.plan(mask, bq, bkv, shapes, head_offset=head_offset, stride_b=0, force_plan=pid, stream=stream)
+        except bsa.BsaError as e:   # e.g. a Split-K workspace that does not fit
+            log("  plan %d not run: %s" % (pid, e))
+            invalid.append(pid)
+            continue
+        if feats is None:
+            info = p.info(0)
+            feats = {"seq_q": N, "seq_kv": N, "batch_heads": bh, "nnz": info["nnz"], "blocks": info["blocks"],
+                     "run_blocks": info["run_blocks"]}
+        ts = []
+        for r in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            bsa.forward(p, q, k, v, o, None, stream=stream)
+            e1.record(stream)
+            e1.synchronize()
+            if r > 0:
+                ts.append(e0.elapsed_time(e1))
+        p.destroy()
+        ok = bool(torch.isfinite(o).all().item())
+        if ok and ref is None:
+            ref = o.clone()
+        elif ok:
+            ok = float((o.float() - ref.float()).abs().max().item()) <= 2e-2
+        if ok:
+            lat[pid] = sorted(ts)[len(ts) // 2]
+        else:
+            invalid.append(pid)
+    del q, k, v, o, mask, ref
+    return {"id": case["id"], "key": [bq, bkv, 0, 128], "family": case["family"], "rho": case["rho"],
+            "features": feats, "latency_ms": {str(p): t for p, t in lat.items()}, "invalid": invalid}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--out", required=True)
+    ap.add_argument("--split", default="profile", choices=sorted(SPLIT_SEED))
+    ap.add_argument("--budget", type=float, default=600.0, help="stop starting new cases after this many seconds")
+    ap.add_argument("--only", default="", help="comma-separated geometries 'bq:bkv' to profile")
+    args = ap.parse_args()
+    import torch
+    import paper_2609_25869_amd as bsa
+
+    done = set()
+    if os.path.exists(args.out):
+        for line in open(args.out):
+            if line.strip():
+                done.add(json.loads(line)["id"])
+    cases = [c for c in corpus(args.split) if c["id"] not in done]
+    if args.only:
+        keep = {tuple(int(x) for x in s.split(":")) for s in args.only.split(",")}
+        cases = [c for c in cases if tuple(c["geometry"]) in keep]
+    log("%d cases to profile (%d already in %s)" % (len(cases), len(done), args.out))
+    t0 = time.time()
+    with open(args.out, "a") as f:
+        for i, c in enumerate(cases):
+            if time.time() - t0 > args.budget:
+                log("budget reached after %d cases" % i)
+                break
+            tc = time.time()
+            rec = profile_case(torch, bsa, c)
+            f.write(json.dumps(rec) + "\n")
+            f.flush()
+            best = min(rec["latency_ms"].items(), key=lambda kv: kv[1])
+            log("%s geom %s N %d bh %d %s %.2f: density %.4f best plan %s %.3f ms, %d invalid (%.1f s)" % (
+                c["id"], c["geometry"], c["N"], c["bh"], c["family"], c["rho"],
+                rec["features"]["nnz"] / rec["features"]["blocks"], best[0], best[1], len(rec["invalid"]),
+                time.time() - tc))
+            torch.cuda.empty_cache()
+    log("done in %.1f s" % (time.time() - t0))
+
+
+if __name__ == "__main__":
+    main()

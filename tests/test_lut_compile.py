@@ -1,0 +1,100 @@
+"""The offline plan table: compilation rules, the shipped artifact, its use by the library (CPU only)."""
+from __future__ import annotations
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+bsa = pytest.importorskip("paper_2609_25869_amd")
+from oracle import regime  # noqa: E402
+from paper_2609_25869_amd.lut import compile as lutc  # noqa: E402
+
+LUT_DIR = os.path.dirname(lutc.__file__)
+ARTIFACT = os.path.join(LUT_DIR, "gfx950_v1.json")
+PROFILE = os.path.join(LUT_DIR, "gfx950_profile.jsonl")
+EVAL = os.path.join(LUT_DIR, "gfx950_eval.jsonl")
+
+
+def base(key):
+    return bsa.base_plan(key[0], key[1])
+
+
+def synthetic_records(seed, n=200):
+    rng = np.random.default_rng(seed)
+    keys = [[64, 64, 0, 128], [128, 128, 0, 128], [16, 16, 0, 128]]
+    recs = []
+    for i in range(n):
+        blocks = int(rng.integers(100, 100000))
+        nnz = int(rng.integers(0, blocks + 1))
+        feats = {"seq_q": int(rng.choice([4096, 65536, 131072])), "seq_kv": 4096,
+                 "batch_heads": int(rng.choice([2, 48])), "nnz": nnz, "blocks": blocks,
+                 "run_blocks": int(rng.integers(0, nnz + 1))}
+        lat = {str(p): float(rng.choice([0.5, 1.0, 1.25, 2.0])) for p in range(24) if rng.random() < 0.85}
+        recs.append({"id": "s%d" % i, "key": keys[i % 3], "features": feats, "latency_ms": lat})
+    return recs
+
+
+def oracle_features(f):
+    return {"seq_q": f["seq_q"], "seq_kv": f["seq_kv"], "batch_heads": f["batch_heads"],
+            "density": (f["nnz"], f["blocks"]), "run_coverage": (f["run_blocks"], f["nnz"])}
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_compile_matches_the_algorithm_restatement(seed):
+    recs = synthetic_records(seed)
+    got = lutc.compile_table(recs, lutc.SCHEMA, base)
+    cases = [{"id": r["id"], "key": tuple(r["key"]), "features": oracle_features(r["features"])} for r in recs]
+    lat = {(r["id"], int(p)): t for r in recs for p, t in r["latency_ms"].items()}
+    want = regime.compile_table(cases, lat, lutc.SCHEMA, base)
+    assert got == want
+
+
+def test_bucket_matches_the_algorithm_restatement():
+    for r in synthetic_records(5, 300):
+        assert lutc.bucket(r["features"], lutc.SCHEMA) == regime.bucket_of(oracle_features(r["features"]), lutc.SCHEMA)
+
+
+def test_shipped_artifact_is_the_compiled_profile():
+    doc = json.load(open(ARTIFACT))
+    table = lutc.compile_table(lutc.load_records(PROFILE), lutc.SCHEMA, base)
+    want = lutc.artifact(table, lutc.SCHEMA, bsa.catalog(), {})
+    assert doc["regimes"] == want["regimes"]
+    assert doc["schema"] == want["schema"] and doc["catalog"] == want["catalog"]
+    assert doc["arch"] == "gfx950" and doc["format"] == "bsa-plan-table" and doc["version"] == 1
+
+
+def test_profile_covers_every_geometry_and_validated_every_plan():
+    recs = lutc.load_records(PROFILE)
+    keys = {tuple(r["key"][:2]) for r in recs}
+    assert {(128, 128), (128, 64), (64, 64), (64, 32), (32, 32), (32, 16), (16, 16), (128, 32), (32, 128)} <= keys
+    for r in recs:
+        eligible = [p for p in range(24) if bsa.plan_eligible(p, r["key"][0], r["key"][1],
+                                                               bsa.make_shapes(1, 1, 1024, 1024))]
+        assert sorted(int(p) for p in r["latency_ms"]) == eligible, r["id"]
+        assert not r.get("invalid")
+
+
+def test_library_uses_the_shipped_table_by_default():
+    """With no table given, the library's lookup equals the artifact's rankings."""
+    table = lutc.compile_table(lutc.load_records(PROFILE), lutc.SCHEMA, base)
+    for r in lutc.load_records(EVAL)[::7]:
+        f = r["features"]
+        z = bsa.regime_query(r["key"][0], r["key"][1], f["batch_heads"], f["seq_q"], f["seq_kv"], f["nnz"],
+                             f["blocks"], f["run_blocks"])
+        ranking, hit = bsa.lut_rank(z)
+        want = table.get(tuple(r["key"]), {}).get(lutc.bucket(f, lutc.SCHEMA))
+        assert hit == (want is not None)
+        assert ranking == (want if want is not None else [base(r["key"])])
+        shapes = bsa.make_shapes(1, f["batch_heads"], f["seq_q"], f["seq_kv"])
+        assert bsa.select_plan(z, shapes) == ranking[0]
+
+
+def test_held_out_selection_regret():
+    """Selected-plan regret on the held-out split (measured latencies, 1 = optimal)."""
+    table = lutc.compile_table(lutc.load_records(PROFILE), lutc.SCHEMA, base)
+    rep = lutc.regret_report(table, lutc.SCHEMA, base, lutc.load_records(EVAL))["all"]
+    assert rep["cases"] >= 200
+    assert rep["gm"] < 1.02 and rep["p95"] < 1.05
