@@ -27,8 +27,12 @@
 //   consecutive rows, one chunk) and V transposed reads (4 rows x 4 chunks
 //   per 16-lane group) then touch distinct bank groups.
 //
-// Numerics: bf16 inputs, fp32 scores and softmax state, scores scaled by
-// log2(e)/sqrt(d) so exp2 is used; P is rounded to bf16 for the PV product;
+// Numerics: bf16 inputs, fp32 scores and softmax state.  The softmax scale
+// log2(e)/sqrt(d) is applied to Q once per task (rounded back to bf16), so
+// the MFMA yields scores in log2 units, and every score accumulator starts
+// at minus the row's current reference: the MFMA output is already the
+// exponent, and a probability costs one exp2.  P is rounded to bf16 for the
+// PV product;
 // O is normalised in fp32 and rounded to bf16 (RNE).  Masked entries
 // (outside the tile's active members, or beyond the sequence end) are -inf
 // before the max; a row whose running max is still -inf uses 0 as its
@@ -102,6 +106,15 @@ __device__ inline void scale_inplace(f32x16& v, float alpha) {
   }
 }
 
+__device__ inline void shift_inplace(f32x16& v, float delta) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    float x = v[i];
+    asm volatile("v_sub_f32_e32 %0, %0, %1" : "+v"(x) : "v"(delta));
+    v[i] = x;
+  }
+}
+
 // x = keep ? x : -inf, in place (keep is per lane)
 __device__ inline void mask_inplace(float& x, bool keep) {
   const float ninf = -__builtin_huge_valf();
@@ -171,17 +184,20 @@ void attn_fwd_kernel(AttnArgs a) {
   const int q0 = task.pq * C::kTQ;
   const int qrow = q0 + 32 * w + n;
 
-  // ---- Q fragment: B operand of S^T = K Q^T, lane (n, hh) holds d = 16c + 8hh .. +8
+  // ---- Q fragment: B operand of S^T = K Q^T, lane (n, hh) holds d = 16c + 8hh .. +8,
+  // pre-multiplied by the softmax scale in log2 units
+  const float c_log2 = a.scale_log2;
   bf16x8 qf[8];
   {
-    const uint16_t* qp = a.q + b * a.qs0 + h * a.qs1 + (int64_t)qrow * a.qs2;
+    // all eight loads are issued before any conversion waits on them
+    const uint16_t* qp = a.q + b * a.qs0 + h * a.qs1 + (int64_t)(qrow < a.Nq ? qrow : 0) * a.qs2;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) qf[c] = *reinterpret_cast<const bf16x8*>(qp + 16 * c + 8 * hh);
+    const float qscale = qrow < a.Nq ? c_log2 : 0.f;
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
-      if (qrow < a.Nq) {
-        qf[c] = *reinterpret_cast<const bf16x8*>(qp + 16 * c + 8 * hh);
-      } else {
-        qf[c] = bf16x8{};
-      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[c][e] = (__bf16)((float)qf[c][e] * qscale);
     }
   }
 
@@ -208,23 +224,37 @@ void attn_fwd_kernel(AttnArgs a) {
   const char* kbase = reinterpret_cast<const char*>(a.k + b * a.ks0 + h * a.ks1);
   const char* vbase = reinterpret_cast<const char*>(a.v + b * a.vs0 + h * a.vs1);
   const int64_t kstride = a.ks2 * 2, vstride = a.vs2 * 2;  // bytes per token
-  uint32_t koffs[kLoadsPerWave], voffs[kLoadsPerWave];
+  // The swizzle depends on the row modulo 16, which repeats every kRep loads
+  // of a wave; later loads reuse those lane offsets and add whole rows
+  // through the scalar offset (which the descriptor's range check includes).
+  constexpr int kRep = NWAVES % 4 == 0 ? 1 : 4 / (NWAVES % 4 == 2 ? 2 : 1);
+  constexpr int kRepN = kRep < kLoadsPerWave ? kRep : kLoadsPerWave;
+  uint32_t koffs[kRepN], voffs[kRepN];
 #pragma unroll
-  for (int j = 0; j < kLoadsPerWave; ++j) {
+  for (int j = 0; j < kRepN; ++j) {
     const int rr = 4 * (w + j * NWAVES) + (lane >> 4);
     const int ch = (lane & 15) ^ swz(rr & 15);
     koffs[j] = (uint32_t)(rr * kstride) + ch * 16;
     voffs[j] = (uint32_t)(rr * vstride) + ch * 16;
   }
+  // descriptor of the TKV tokens starting at kv0
+  auto tile_rsrc = [&](const char* base, int64_t stride, int kv0) {
+    const int rows = min(TKV, a.Nkv - kv0);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base + (int64_t)kv0 * stride), 0,
+                                             (int)(rows * stride), 0x00020000);
+  };
+  // load j of this wave's share of one tile
+  auto dma_one = [&](__amdgpu_buffer_rsrc_t rsrc, int64_t stride, const uint32_t* offs, int j, uint8_t* dst_arr) {
+    const int soff = (j / kRep) * (kRep * 4 * NWAVES) * (int)stride;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rsrc, (__attribute__((address_space(3))) void*)(dst_arr + 1024 * (w + j * NWAVES)), 16, offs[j % kRep], soff,
+        0, 0);
+  };
   // copy the TKV tokens starting at kv0 into one ring slot
   auto dma_rows = [&](const char* base, int64_t stride, const uint32_t* offs, int kv0, uint8_t* dst_arr) {
-    const int rows = min(TKV, a.Nkv - kv0);
-    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<char*>(base + (int64_t)kv0 * stride), 0, (int)(rows * stride), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsrc = tile_rsrc(base, stride, kv0);
 #pragma unroll
-    for (int j = 0; j < kLoadsPerWave; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rsrc, (__attribute__((address_space(3))) void*)(dst_arr + 1024 * (w + j * NWAVES)), 16, offs[j], 0, 0, 0);
+    for (int j = 0; j < kLoadsPerWave; ++j) dma_one(rsrc, stride, offs, j, dst_arr);
   };
   auto dma_k = [&](int kv0, int slot) { dma_rows(kbase, kstride, koffs, kv0, kslot(slot)); };
   auto dma_v = [&](int kv0, int slot) { dma_rows(vbase, vstride, voffs, kv0, vslot(slot)); };
@@ -255,13 +285,15 @@ void attn_fwd_kernel(AttnArgs a) {
   const int mem_row = (a.gq > 1) ? (q_local >> a.bq_shift) : 0;
   const int mem_bits = a.gq * a.gkv;
   const uint64_t full = (mem_bits >= 64) ? ~0ull : ((1ull << mem_bits) - 1);
-  const float c_log2 = a.scale_log2;
   const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
   f32x16 o[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) o[i] = f32x16{};
   float m_run = kNegInf, l_run = 0.f;
+  // minus the reference, broadcast: the initial accumulator of every score
+  // MFMA chain (changed only when the reference is raised)
+  f32x16 negm = f32x16{};
 
   // MFMA operand stream of one iteration: units [0, kNA) are the S^T MFMAs of
   // the next tile (A = K rows), units [kNA, kNU) the O^T MFMAs of this tile
@@ -323,8 +355,8 @@ void attn_fwd_kernel(AttnArgs a) {
     }
   };
 
-  // Row maximum of one tile's raw scores (the scale is positive), both lane
-  // halves combined.
+  // Row maximum of one tile's scores (relative to the reference they were
+  // computed against), both lane halves combined.
   auto row_max = [&](const f32x16* s) -> float {
     float mx = kNegInf;
 #pragma unroll
@@ -336,57 +368,88 @@ void attn_fwd_kernel(AttnArgs a) {
   };
 
   // Distribution of the VALU work of one iteration over its MFMA units.
-  // Probabilities of all but the last 8-key chunk are formed during the
-  // S^T units (which have spare VALU slots); the last chunk during the first
-  // O^T units, before its MFMAs; the row maximum of the next tile's scores
-  // during the remaining O^T units, so the next iteration starts with it.
-  constexpr int kE = 16 * kNKB;         // score elements per lane
-  constexpr int kChunks = TKV / 16;     // 8-element P chunks
-  constexpr int kP = kE - 8;            // elements formed during the S^T units
+  // A probability is made in two steps one unit apart: the exponential
+  // (stage A) and, for a pair of them, the bf16 packing and the row-sum dot
+  // product (stage B), so no unit waits on an exponential it just issued.
+  // Stage A covers all but the last 8-key chunk during the first kQA S^T
+  // units and the last chunk during the first kJA O^T units, ahead of the
+  // MFMAs that consume it; the row maximum of the next tile's scores is
+  // formed during the O^T units from kMx0 on, so the next iteration starts
+  // with it.
+  constexpr int kE = 16 * kNKB;           // score elements per lane
+  constexpr int kChunks = TKV / 16;       // 8-element P chunks
+  constexpr int kP = kE - 8;              // stage-A elements of the S^T units
+  constexpr int kQA = kNA - 1;            // S^T units with stage-A work
   constexpr int kJ1 = 4 * (kChunks - 1);  // first O^T unit that needs the last chunk
-  constexpr int kMx0 = 2;               // first O^T unit doing max steps
-  constexpr int kNmx = kE / 2;          // pairwise max steps
-  static_assert(kChunks >= 2, "pipeline needs two P chunks");
+  constexpr int kJA = kJ1 - 1;            // O^T units with stage-A work
+  constexpr int kMx0 = 2;                 // first O^T unit doing max steps
+  constexpr int kGroupLoads = 2 * kLoadsPerWave;  // refill loads of one iteration
+  constexpr int kDmaEvery = kNU / kGroupLoads;
+  static_assert(kDmaEvery >= 1 && kDmaEvery * kGroupLoads <= kNU, "refill loads must fit the units");
+  constexpr int kNmx = kE / 2;            // pairwise max steps
+  static_assert(kChunks >= 2 && kJA >= 2, "pipeline needs two P chunks");
 
   // One pipeline iteration over tile t: (rare) mask and max of s_cur, the
-  // reference update; then the S^T MFMAs of the next tile (from ks_next)
-  // interleaved with the probabilities of this tile, and the O^T MFMAs of
-  // this tile (V from vs_cur) interleaved with the rest of them and with the
-  // row maximum of the next tile.  Returns that maximum (raw scores).
+  // reference update; then the S^T MFMAs of the next tile (from ks_next,
+  // accumulators starting at minus the updated reference) interleaved with
+  // the probabilities of this tile, and the O^T MFMAs of this tile (V from
+  // vs_cur) interleaved with the rest of them and with the row maximum of
+  // the next tile.  s_cur holds scores minus m_ref, the reference in force
+  // when its MFMAs began (0 while the row has seen no score); mx_cur is its
+  // maximum.  Returns the maximum of the next tile's scores, relative to the
+  // reference after this iteration's update.
   auto iteration = [&](f32x16* s_cur, f32x16* s_nxt, float mx_cur, int kv0_cur, uint64_t bits_cur,
-                       const uint8_t* ks_next, const uint8_t* vs_cur) -> float {
+                       const uint8_t* ks_next, const uint8_t* vs_cur, int kv0_refill_k, int kv0_refill_v,
+                       uint8_t* k_refill, uint8_t* v_refill) -> float {
+    // the ring refill of this iteration, one load every kDmaEvery units
+    const __amdgpu_buffer_rsrc_t rk = tile_rsrc(kbase, kstride, kv0_refill_k);
+    const __amdgpu_buffer_rsrc_t rv = tile_rsrc(vbase, vstride, kv0_refill_v);
     if (__builtin_expect(kv0_cur + TKV > a.Nkv || bits_cur != full, 0)) {
       apply_mask(s_cur, kv0_cur, bits_cur);
       mx_cur = row_max(s_cur);
     }
-    const float mxs = mx_cur * c_log2;
-    // raise the reference only when needed (wave-uniform branch)
-    const bool need = mxs > m_run + kTau;
+    const float m_ref = (m_run == kNegInf) ? 0.f : m_run;
+    const float mx_abs = mx_cur + m_ref;
+    // raise the reference only when needed (wave-uniform branch); the
+    // scores of this tile then move to the new reference as well
+    const bool need = mx_abs > m_run + kTau;
     if (__ballot(need)) {
-      const float m_new = need ? mxs : m_run;
+      const float m_new = need ? mx_abs : m_run;
       const float alpha = need ? fast_exp2(m_run - m_new) : 1.f;
+      const float delta = need ? m_new - m_ref : 0.f;
       m_run = m_new;
       l_run *= alpha;
 #pragma unroll
       for (int d = 0; d < 4; ++d) scale_inplace(o[d], alpha);
-    }
-    const float nm = (m_run == kNegInf) ? 0.f : -m_run;
-
 #pragma unroll
-    for (int kb = 0; kb < kNKB; ++kb) s_nxt[kb] = f32x16{};
+      for (int kb = 0; kb < kNKB; ++kb) shift_inplace(s_cur[kb], delta);
+      const float nm = (m_run == kNegInf) ? 0.f : -m_run;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) negm[i] = nm;
+    }
     // row sums of the bf16 probabilities (the weights PV actually uses)
     float ls0 = 0.f, ls1 = 0.f;
     float mxa = kNegInf, mxb = kNegInf;
+    float pf[kE];
     bf16x8 pb[kChunks];
-    // probability of element ei (chunk ei / 8, slot ei % 8 of that chunk)
-    auto prob = [&](int ei) {
-      const float p = fast_exp2(__builtin_fmaf(s_cur[ei / 16][ei % 16], c_log2, nm));
-      pb[ei / 8][ei % 8] = (__bf16)p;
-      if (ei & 1) {
-        const bf16x2 pair = {pb[ei / 8][(ei % 8) - 1], pb[ei / 8][ei % 8]};
-        if (ei & 2) ls1 = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, ls1, false);
-        else ls0 = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, ls0, false);
-      }
+    // elements whose exponential is formed by the end of unit uu
+    auto a_end = [&](int uu) -> int {
+      return uu < 0 ? 0
+           : uu < kQA ? (uu + 1) * kP / kQA
+           : uu < kNA ? kP
+           : uu < kNA + kJA ? kP + (uu - kNA + 1) * (kE - kP) / kJA
+           : kE;
+    };
+    auto stage_a = [&](int ei) {
+      pf[ei] = fast_exp2(s_cur[ei / 16][ei % 16]);
+    };
+    auto stage_b = [&](int pr) {
+      const int e0 = 2 * pr;
+      pb[e0 / 8][e0 % 8] = (__bf16)pf[e0];
+      pb[e0 / 8][e0 % 8 + 1] = (__bf16)pf[e0 + 1];
+      const bf16x2 pair = {pb[e0 / 8][e0 % 8], pb[e0 / 8][e0 % 8 + 1]};
+      if (pr & 1) ls1 = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, ls1, false);
+      else ls0 = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, ls0, false);
     };
     // max step k covers elements 2k and 2k+1 of the next tile
     auto max_step = [&](int k) {
@@ -394,30 +457,33 @@ void attn_fwd_kernel(AttnArgs a) {
       float& acc = (k & 1) ? mxb : mxa;
       acc = fmaxf(acc, fmaxf(s_nxt[e0 / 16][e0 % 16], s_nxt[(e0 + 1) / 16][(e0 + 1) % 16]));
     };
-    constexpr int kAhead = 3;  // operand read distance, in units
+    constexpr int kAhead = 2;  // operand read distance, in units
     bf16x8 op[kAhead + 1];
 #pragma unroll
     for (int u = 0; u < kAhead; ++u) op[u] = load_op(u, ks_next, vs_cur);
 #pragma unroll
     for (int u = 0; u < kNU; ++u) {
       if (u + kAhead < kNU) op[(u + kAhead) % (kAhead + 1)] = load_op(u + kAhead, ks_next, vs_cur);
+      if (u % kDmaEvery == 0 && u / kDmaEvery < kGroupLoads) {
+        const int i = u / kDmaEvery;
+        if (i < kLoadsPerWave) dma_one(rk, kstride, koffs, i, k_refill);
+        else dma_one(rv, vstride, voffs, i - kLoadsPerWave, v_refill);
+      }
       if (u < kNA) {
-        s_nxt[u % kNKB] = mfma32(op[u % (kAhead + 1)], qf[u / kNKB], s_nxt[u % kNKB]);
-#pragma unroll
-        for (int e = u * kP / kNA; e < (u + 1) * kP / kNA; ++e) prob(e);
+        s_nxt[u % kNKB] = mfma32(op[u % (kAhead + 1)], qf[u / kNKB], u < kNKB ? negm : s_nxt[u % kNKB]);
       } else {
         const int j = u - kNA;
         o[j % 4] = mfma32(op[u % (kAhead + 1)], pb[j / 4], o[j % 4]);
-        if (j < kJ1) {
-#pragma unroll
-          for (int e = kP + j * 8 / kJ1; e < kP + (j + 1) * 8 / kJ1; ++e) prob(e);
-        }
         if (j >= kMx0) {
           const int jj = j - kMx0, nj = kNB - kMx0;
 #pragma unroll
           for (int k = jj * kNmx / nj; k < (jj + 1) * kNmx / nj; ++k) max_step(k);
         }
       }
+#pragma unroll
+      for (int pr = a_end(u - 2) / 2; pr < a_end(u - 1) / 2; ++pr) stage_b(pr);
+#pragma unroll
+      for (int e = a_end(u - 1); e < a_end(u); ++e) stage_a(e);
       __builtin_amdgcn_sched_barrier(0);
     }
     l_run += ls0 + ls1;
@@ -465,11 +531,11 @@ void attn_fwd_kernel(AttnArgs a) {
       const int t = t0 + u;
       if (t >= nkv_tiles) break;
       // refill slot t % STAGES with K of tile t+STAGES and V of tile t+STAGES-1
-      dma_k(kv_next_k, u);
-      dma_v(kv_next_v, u);
+      // (issued inside the iteration, spread over its MFMA units)
       f32x16* s_cur = (u % 2 == 0) ? sA : sB;
       f32x16* s_nxt = (u % 2 == 0) ? sB : sA;
-      mx_cur = iteration(s_cur, s_nxt, mx_cur, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES));
+      mx_cur = iteration(s_cur, s_nxt, mx_cur, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES),
+                         kv_next_k, kv_next_v, kslot(u), vslot(u));
       // scalars of the next iteration, complete before the barrier so no
       // scalar load is outstanding while the next iteration's LDS reads are
       // counted
