@@ -3,7 +3,8 @@
 // TKV tokens streamed through LDS rings of STAGES slots (pipeline depth,
 // Sections 2.3, 4.2, 4.3).  The loop is software pipelined: the scores of
 // tile t+1 (MFMA) are computed while the probabilities of tile t (VALU) are
-// formed, then O accumulates P V of tile t.
+// formed and O accumulates P V of tile t-1, whose probabilities were
+// checked at the end of the previous iteration.
 //
 // Layout of the work inside a wavefront
 //   The score tile is computed transposed, S^T = K Q^T, with
@@ -27,16 +28,17 @@
 //   consecutive rows, one chunk) and V transposed reads (4 rows x 4 chunks
 //   per 16-lane group) then touch distinct bank groups.
 //
-// Numerics: bf16 inputs, fp32 scores and softmax state.  The softmax scale
-// log2(e)/sqrt(d) is applied to Q once per task (rounded back to bf16), so
-// the MFMA yields scores in log2 units, and every score accumulator starts
-// at minus the row's current reference: the MFMA output is already the
-// exponent, and a probability costs one exp2.  P is rounded to bf16 for the
-// PV product;
-// O is normalised in fp32 and rounded to bf16 (RNE).  Masked entries
-// (outside the tile's active members, or beyond the sequence end) are -inf
-// before the max; a row whose running max is still -inf uses 0 as its
-// reference so no NaN can arise (it keeps l = 0 and O = 0).
+// Numerics: bf16 inputs, fp32 scores and softmax state, scores scaled by
+// log2(e)/sqrt(d) in fp32 so exp2 is used.  The running reference m of a
+// row is not tracked tile by tile: the probabilities of a tile are formed
+// against the current reference and their sum is checked before any MFMA
+// consumes them; only when a probability may exceed 2^kTau (or the row has
+// no reference yet) is the tile's row maximum formed, the reference raised
+// and O rescaled.  P is rounded to bf16 for the PV product; O is normalised
+// in fp32 and rounded to bf16 (RNE).  Masked entries (outside the tile's
+// active members, or beyond the sequence end) are -inf before any of this;
+// a row whose reference is still unset uses 0 as its reference, so no NaN
+// can arise (it keeps l = 0 and O = 0).
 #include "bsa_internal.h"
 
 namespace bsa {
@@ -49,6 +51,7 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
@@ -106,26 +109,18 @@ __device__ inline void scale_inplace(f32x16& v, float alpha) {
   }
 }
 
-__device__ inline void shift_inplace(f32x16& v, float delta) {
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    float x = v[i];
-    asm volatile("v_sub_f32_e32 %0, %0, %1" : "+v"(x) : "v"(delta));
-    v[i] = x;
-  }
-}
-
 // x = keep ? x : -inf, in place (keep is per lane)
 __device__ inline void mask_inplace(float& x, bool keep) {
   const float ninf = -__builtin_huge_valf();
   asm volatile("v_cndmask_b32_e64 %0, %1, %0, %2" : "+v"(x) : "v"(ninf), "s"(__ballot(keep)));
 }
 
-// The running maximum is only raised when a tile's maximum exceeds it by more
-// than kTau (log2 units).  Until then probabilities are computed against the
-// old reference and stay below 2^kTau, which fp32 sums and bf16 P hold
-// exactly as well; the rescale of O is skipped for most tiles.
+// The reference of a row is only raised when the probabilities of a tile,
+// formed against it, sum to more than 2^kTau in one lane; below that every
+// probability is at most 2^kTau, which fp32 sums and bf16 P hold exactly as
+// well, and the rescale of O is skipped.
 constexpr float kTau = 8.0f;
+constexpr float kSumMax = 256.0f;  // 2^kTau
 
 // Wait until at most N of this wave's vector-memory operations (the LDS DMA
 // of younger tiles) are outstanding and all of its LDS reads have retired
@@ -153,12 +148,12 @@ void attn_fwd_kernel(AttnArgs a) {
   using C = Cfg<NWAVES, TKV>;
   constexpr int kNKB = C::kNKB;
   static_assert(STAGES == 2 || STAGES == 4, "ring depth");
-  // A ring of STAGES slots; slot j holds a K tile and a V tile.  Iteration t
-  // consumes slot (t+1) % STAGES, which holds K of tile t+1 (scores of the
-  // next tile) and V of tile t (this tile's output), and refills slot
-  // t % STAGES (consumed by iteration t-1) with K of tile t+STAGES and V of
-  // tile t+STAGES-1, so every load has STAGES-2 whole iterations plus the
-  // current one to arrive.  Each slot is its own array: the compiler then
+  // A ring of STAGES slots; slot j holds K of a tile x = j (mod STAGES) and
+  // V of tile x-2.  Iteration t reads slot (t+1) % STAGES: K of tile t+1
+  // (scores of the next tile) and V of tile t-1 (O += P V of the previous
+  // tile), and refills slot t % STAGES (read by iteration t-1) with K of
+  // tile t+STAGES and V of tile t+STAGES-2, so every load has STAGES-2 whole
+  // iterations plus the current one to arrive.  Each slot is its own array: the compiler then
   // sees that reads of one slot never alias the DMA filling another and
   // keeps those loads in flight.
   constexpr int kSlotBytes = 2 * C::kTileBytes;
@@ -184,20 +179,16 @@ void attn_fwd_kernel(AttnArgs a) {
   const int q0 = task.pq * C::kTQ;
   const int qrow = q0 + 32 * w + n;
 
-  // ---- Q fragment: B operand of S^T = K Q^T, lane (n, hh) holds d = 16c + 8hh .. +8,
-  // pre-multiplied by the softmax scale in log2 units
+  // ---- Q fragment: B operand of S^T = K Q^T, lane (n, hh) holds d = 16c + 8hh .. +8
   const float c_log2 = a.scale_log2;
   bf16x8 qf[8];
   {
-    // all eight loads are issued before any conversion waits on them
     const uint16_t* qp = a.q + b * a.qs0 + h * a.qs1 + (int64_t)(qrow < a.Nq ? qrow : 0) * a.qs2;
 #pragma unroll
     for (int c = 0; c < 8; ++c) qf[c] = *reinterpret_cast<const bf16x8*>(qp + 16 * c + 8 * hh);
-    const float qscale = qrow < a.Nq ? c_log2 : 0.f;
+    if (qrow >= a.Nq) {
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qf[c][e] = (__bf16)((float)qf[c][e] * qscale);
+      for (int c = 0; c < 8; ++c) qf[c] = bf16x8{};
     }
   }
 
@@ -258,8 +249,8 @@ void attn_fwd_kernel(AttnArgs a) {
   };
   auto dma_k = [&](int kv0, int slot) { dma_rows(kbase, kstride, koffs, kv0, kslot(slot)); };
   auto dma_v = [&](int kv0, int slot) { dma_rows(vbase, vstride, voffs, kv0, vslot(slot)); };
-  // first token of tile t, clamped to the task's last tile
-  auto tile_kv0 = [&](int t) -> int { return kvt[t < nkv_tiles ? t : nkv_tiles - 1] * TKV; };
+  // first token of tile t, clamped to the task's tiles
+  auto tile_kv0 = [&](int t) -> int { return kvt[t < 0 ? 0 : t < nkv_tiles ? t : nkv_tiles - 1] * TKV; };
 
   // lane-constant LDS offsets
   const int sw = swz(lane & 15);
@@ -291,9 +282,6 @@ void attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) o[i] = f32x16{};
   float m_run = kNegInf, l_run = 0.f;
-  // minus the reference, broadcast: the initial accumulator of every score
-  // MFMA chain (changed only when the reference is raised)
-  f32x16 negm = f32x16{};
 
   // MFMA operand stream of one iteration: units [0, kNA) are the S^T MFMAs of
   // the next tile (A = K rows), units [kNA, kNU) the O^T MFMAs of this tile
@@ -326,8 +314,9 @@ void attn_fwd_kernel(AttnArgs a) {
     }
   };
 
-  // entries outside the tile's active members or past the sequence end -> -inf
-  auto apply_mask = [&](f32x16* s, int kv0, uint64_t bits) {
+  // entries outside the tile's active members or past the sequence end ->
+  // -inf; returns whether this lane's row keeps any key of the tile
+  auto apply_mask = [&](f32x16* s, int kv0, uint64_t bits) -> bool {
     const uint64_t rowbits = bits >> (mem_row * a.gkv);
     // allowed-key bitmap of this lane's row over the tile
     uint64_t allowed = 0;
@@ -353,10 +342,11 @@ void attn_fwd_kernel(AttnArgs a) {
         s[kb][i] = x;
       }
     }
+    return allowed != 0;
   };
 
-  // Row maximum of one tile's scores (relative to the reference they were
-  // computed against), both lane halves combined.
+  // Row maximum of one tile's raw scores (the scale is positive), both lane
+  // halves combined.
   auto row_max = [&](const f32x16* s) -> float {
     float mx = kNegInf;
 #pragma unroll
@@ -371,114 +361,65 @@ void attn_fwd_kernel(AttnArgs a) {
   // A probability is made in two steps one unit apart: the exponential
   // (stage A) and, for a pair of them, the bf16 packing and the row-sum dot
   // product (stage B), so no unit waits on an exponential it just issued.
-  // Stage A covers all but the last 8-key chunk during the first kQA S^T
-  // units and the last chunk during the first kJA O^T units, ahead of the
-  // MFMAs that consume it; the row maximum of the next tile's scores is
-  // formed during the O^T units from kMx0 on, so the next iteration starts
-  // with it.
+  // Stage A is spread over all but the last unit; none of it feeds an MFMA
+  // of the same iteration.
   constexpr int kE = 16 * kNKB;           // score elements per lane
   constexpr int kChunks = TKV / 16;       // 8-element P chunks
-  constexpr int kP = kE - 8;              // stage-A elements of the S^T units
-  constexpr int kQA = kNA - 1;            // S^T units with stage-A work
-  constexpr int kJ1 = 4 * (kChunks - 1);  // first O^T unit that needs the last chunk
-  constexpr int kJA = kJ1 - 1;            // O^T units with stage-A work
-  constexpr int kMx0 = 2;                 // first O^T unit doing max steps
   constexpr int kGroupLoads = 2 * kLoadsPerWave;  // refill loads of one iteration
   constexpr int kDmaEvery = kNU / kGroupLoads;
   static_assert(kDmaEvery >= 1 && kDmaEvery * kGroupLoads <= kNU, "refill loads must fit the units");
-  constexpr int kNmx = kE / 2;            // pairwise max steps
-  static_assert(kChunks >= 2 && kJA >= 2, "pipeline needs two P chunks");
+  // elements whose exponential is formed by the end of unit uu
+  auto a_end = [&](int uu) -> int { return uu < 0 ? 0 : uu < kNU - 1 ? (uu + 1) * kE / (kNU - 1) : kE; };
+  constexpr int kAhead = 3;  // operand read distance, in units
 
-  // One pipeline iteration over tile t: (rare) mask and max of s_cur, the
-  // reference update; then the S^T MFMAs of the next tile (from ks_next,
-  // accumulators starting at minus the updated reference) interleaved with
-  // the probabilities of this tile, and the O^T MFMAs of this tile (V from
-  // vs_cur) interleaved with the rest of them and with the row maximum of
-  // the next tile.  s_cur holds scores minus m_ref, the reference in force
-  // when its MFMAs began (0 while the row has seen no score); mx_cur is its
-  // maximum.  Returns the maximum of the next tile's scores, relative to the
-  // reference after this iteration's update.
-  auto iteration = [&](f32x16* s_cur, f32x16* s_nxt, float mx_cur, int kv0_cur, uint64_t bits_cur,
-                       const uint8_t* ks_next, const uint8_t* vs_cur, int kv0_refill_k, int kv0_refill_v,
-                       uint8_t* k_refill, uint8_t* v_refill) -> float {
+  // probability of a raw score against the reference -nm, and the bf16
+  // packing of a pair of them (register k of chunk c holds elements 8c + 2k
+  // and 8c + 2k + 1)
+  auto exponent = [&](float sv, float nm) { return fast_exp2(__builtin_fmaf(sv, c_log2, nm)); };
+  auto pack_pair = [&](float p0, float p1) { return __builtin_convertvector((f32x2){p0, p1}, bf16x2); };
+
+  // One pipeline iteration over tile t: (rare) masking of s_cur; the S^T
+  // MFMAs of tile t+1 (K from ks_next) and the O^T MFMAs of tile t-1 (V from
+  // vs_prev, P from pw_prev) interleaved with the probabilities of tile t
+  // (into pw_cur).  Returns the lane's sum of those probabilities; active
+  // tells whether the lane's row has a key in tile t.
+  auto iteration = [&](f32x16* s_cur, f32x16* s_nxt, int kv0_cur, uint64_t bits_cur, const uint8_t* ks_next,
+                       const uint8_t* vs_prev, u32x4* pw_cur, const u32x4* pw_prev, int kv0_refill_k,
+                       int kv0_refill_v, uint8_t* k_refill, uint8_t* v_refill, bool& active) -> float {
     // the ring refill of this iteration, one load every kDmaEvery units
     const __amdgpu_buffer_rsrc_t rk = tile_rsrc(kbase, kstride, kv0_refill_k);
     const __amdgpu_buffer_rsrc_t rv = tile_rsrc(vbase, vstride, kv0_refill_v);
-    if (__builtin_expect(kv0_cur + TKV > a.Nkv || bits_cur != full, 0)) {
-      apply_mask(s_cur, kv0_cur, bits_cur);
-      mx_cur = row_max(s_cur);
-    }
-    const float m_ref = (m_run == kNegInf) ? 0.f : m_run;
-    const float mx_abs = mx_cur + m_ref;
-    // raise the reference only when needed (wave-uniform branch); the
-    // scores of this tile then move to the new reference as well
-    const bool need = mx_abs > m_run + kTau;
-    if (__ballot(need)) {
-      const float m_new = need ? mx_abs : m_run;
-      const float alpha = need ? fast_exp2(m_run - m_new) : 1.f;
-      const float delta = need ? m_new - m_ref : 0.f;
-      m_run = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int d = 0; d < 4; ++d) scale_inplace(o[d], alpha);
-#pragma unroll
-      for (int kb = 0; kb < kNKB; ++kb) shift_inplace(s_cur[kb], delta);
-      const float nm = (m_run == kNegInf) ? 0.f : -m_run;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) negm[i] = nm;
-    }
-    // row sums of the bf16 probabilities (the weights PV actually uses)
+    active = true;
+    if (__builtin_expect(kv0_cur + TKV > a.Nkv || bits_cur != full, 0)) active = apply_mask(s_cur, kv0_cur, bits_cur);
+    const float nm = (m_run == kNegInf) ? 0.f : -m_run;
     float ls0 = 0.f, ls1 = 0.f;
-    float mxa = kNegInf, mxb = kNegInf;
     float pf[kE];
-    bf16x8 pb[kChunks];
-    // elements whose exponential is formed by the end of unit uu
-    auto a_end = [&](int uu) -> int {
-      return uu < 0 ? 0
-           : uu < kQA ? (uu + 1) * kP / kQA
-           : uu < kNA ? kP
-           : uu < kNA + kJA ? kP + (uu - kNA + 1) * (kE - kP) / kJA
-           : kE;
-    };
-    auto stage_a = [&](int ei) {
-      pf[ei] = fast_exp2(s_cur[ei / 16][ei % 16]);
-    };
+    auto stage_a = [&](int ei) { pf[ei] = exponent(s_cur[ei / 16][ei % 16], nm); };
     auto stage_b = [&](int pr) {
       const int e0 = 2 * pr;
-      pb[e0 / 8][e0 % 8] = (__bf16)pf[e0];
-      pb[e0 / 8][e0 % 8 + 1] = (__bf16)pf[e0 + 1];
-      const bf16x2 pair = {pb[e0 / 8][e0 % 8], pb[e0 / 8][e0 % 8 + 1]};
-      if (pr & 1) ls1 = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, ls1, false);
-      else ls0 = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, ls0, false);
+      const bf16x2 pair = pack_pair(pf[e0], pf[e0 + 1]);
+      pw_cur[e0 / 8][(e0 % 8) / 2] = __builtin_bit_cast(uint32_t, pair);
+      float& acc = (pr & 1) ? ls1 : ls0;
+      acc = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, acc, false);
+      // keep the sum in this unit (otherwise it is sunk to the end of the loop)
+      asm volatile("" : "+v"(acc));
     };
-    // max step k covers elements 2k and 2k+1 of the next tile
-    auto max_step = [&](int k) {
-      const int e0 = 2 * k;
-      float& acc = (k & 1) ? mxb : mxa;
-      acc = fmaxf(acc, fmaxf(s_nxt[e0 / 16][e0 % 16], s_nxt[(e0 + 1) / 16][(e0 + 1) % 16]));
-    };
-    constexpr int kAhead = 2;  // operand read distance, in units
     bf16x8 op[kAhead + 1];
 #pragma unroll
-    for (int u = 0; u < kAhead; ++u) op[u] = load_op(u, ks_next, vs_cur);
+    for (int u = 0; u < kAhead; ++u) op[u] = load_op(u, ks_next, vs_prev);
 #pragma unroll
     for (int u = 0; u < kNU; ++u) {
-      if (u + kAhead < kNU) op[(u + kAhead) % (kAhead + 1)] = load_op(u + kAhead, ks_next, vs_cur);
+      if (u + kAhead < kNU) op[(u + kAhead) % (kAhead + 1)] = load_op(u + kAhead, ks_next, vs_prev);
       if (u % kDmaEvery == 0 && u / kDmaEvery < kGroupLoads) {
         const int i = u / kDmaEvery;
         if (i < kLoadsPerWave) dma_one(rk, kstride, koffs, i, k_refill);
         else dma_one(rv, vstride, voffs, i - kLoadsPerWave, v_refill);
       }
       if (u < kNA) {
-        s_nxt[u % kNKB] = mfma32(op[u % (kAhead + 1)], qf[u / kNKB], u < kNKB ? negm : s_nxt[u % kNKB]);
+        s_nxt[u % kNKB] = mfma32(op[u % (kAhead + 1)], qf[u / kNKB], u < kNKB ? f32x16{} : s_nxt[u % kNKB]);
       } else {
         const int j = u - kNA;
-        o[j % 4] = mfma32(op[u % (kAhead + 1)], pb[j / 4], o[j % 4]);
-        if (j >= kMx0) {
-          const int jj = j - kMx0, nj = kNB - kMx0;
-#pragma unroll
-          for (int k = jj * kNmx / nj; k < (jj + 1) * kNmx / nj; ++k) max_step(k);
-        }
+        o[j % 4] = mfma32(op[u % (kAhead + 1)], __builtin_bit_cast(bf16x8, pw_prev[j / 4]), o[j % 4]);
       }
 #pragma unroll
       for (int pr = a_end(u - 2) / 2; pr < a_end(u - 1) / 2; ++pr) stage_b(pr);
@@ -486,9 +427,33 @@ void attn_fwd_kernel(AttnArgs a) {
       for (int e = a_end(u - 1); e < a_end(u); ++e) stage_a(e);
       __builtin_amdgcn_sched_barrier(0);
     }
-    l_run += ls0 + ls1;
-    const float mx_next = fmaxf(mxa, mxb);
-    return fmaxf(mx_next, other_half(mx_next));
+    return ls0 + ls1;
+  };
+
+  // Rare path after an iteration: a probability of tile t may exceed 2^kTau
+  // (or some row met its first key).  Raise each row's reference to the
+  // maximum of its scores so far, rescale O and l, and form the tile's
+  // probabilities again.  O holds P V up to tile t-1, all against the old
+  // reference, so one factor per row covers it.
+  auto raise_reference = [&](const f32x16* s_cur, u32x4* pw_cur) -> float {
+    const float mxs = row_max(s_cur) * c_log2;
+    const float m_new = fmaxf(m_run, mxs);
+    const float alpha = (m_new == m_run) ? 1.f : fast_exp2(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) scale_inplace(o[d], alpha);
+    const float nm = (m_run == kNegInf) ? 0.f : -m_run;
+    float ls = 0.f;
+#pragma unroll
+    for (int pr = 0; pr < kE / 2; ++pr) {
+      const int e0 = 2 * pr;
+      const bf16x2 pair =
+          pack_pair(exponent(s_cur[e0 / 16][e0 % 16], nm), exponent(s_cur[e0 / 16][e0 % 16 + 1], nm));
+      pw_cur[e0 / 8][(e0 % 8) / 2] = __builtin_bit_cast(uint32_t, pair);
+      ls = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, ls, false);
+    }
+    return ls;
   };
 
   // number of DMA instructions one iteration issues (K tile and V tile)
@@ -496,31 +461,33 @@ void attn_fwd_kernel(AttnArgs a) {
   constexpr int kInFlight = (STAGES - 2) * kGroup;
 
   f32x16 sA[kNKB], sB[kNKB];
-  float mx_cur = kNegInf;  // row maximum of the scores of the current tile
+  u32x4 pwA[kChunks], pwB[kChunks];
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) pwB[c] = u32x4{};  // P of "tile -1": no contribution
   // scalars for the coming iteration, fetched one iteration ahead
   int kv_next_k = 0, kv_next_v = 0, kv_cur = 0;
   uint64_t bits_cur = full;
   if (nkv_tiles > 0) {
     // prologue: K of tile 0 into slot 0, then slot j <- (K of tile j, V of
-    // tile j-1) for j = 1..STAGES-1, in the order they are needed.  Ring
-    // refills are never skipped: past the end of the task they re-load its
-    // last tile into the free slot, which keeps the count of loads in flight
-    // the same on every path.
+    // tile j-2) for j = 1..STAGES-1, in the order they are needed (V of the
+    // "tile -1" that iteration 0 multiplies by zero probabilities is tile 0,
+    // any finite data).  Ring refills are never skipped: past the end of the
+    // task they re-load its last tile into the free slot, which keeps the
+    // count of loads in flight the same on every path.
     dma_k(tile_kv0(0), 0);
 #pragma unroll
     for (int j = 1; j < STAGES; ++j) {
       dma_k(tile_kv0(j), j);
-      dma_v(tile_kv0(j - 1), j);
+      dma_v(tile_kv0(j - 2), j);
     }
     kv_next_k = tile_kv0(STAGES);
-    kv_next_v = tile_kv0(STAGES - 1);
+    kv_next_v = tile_kv0(STAGES - 2);
     kv_cur = tile_kv0(0);
     bits_cur = mbits ? mbits[0] : full;
     // the scores of tile 0 need K0 only
     wait_vm_lgkm<(STAGES - 1) * kGroup>();
     block_sync();
     qk_only(kslot(0), sA);
-    mx_cur = row_max(sA);
     // the first iteration needs slot 1
     wait_vm_lgkm<kInFlight>();
     block_sync();  // every wave has read slot 0 before it is refilled
@@ -530,17 +497,24 @@ void attn_fwd_kernel(AttnArgs a) {
     for (int u = 0; u < STAGES; ++u) {
       const int t = t0 + u;
       if (t >= nkv_tiles) break;
-      // refill slot t % STAGES with K of tile t+STAGES and V of tile t+STAGES-1
-      // (issued inside the iteration, spread over its MFMA units)
+      // refill slot t % STAGES with K of tile t+STAGES and V of tile
+      // t+STAGES-2 (issued inside the iteration, spread over its MFMA units)
       f32x16* s_cur = (u % 2 == 0) ? sA : sB;
       f32x16* s_nxt = (u % 2 == 0) ? sB : sA;
-      mx_cur = iteration(s_cur, s_nxt, mx_cur, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES),
-                         kv_next_k, kv_next_v, kslot(u), vslot(u));
+      u32x4* pw_cur = (u % 2 == 0) ? pwA : pwB;
+      u32x4* pw_prev = (u % 2 == 0) ? pwB : pwA;
+      bool active;
+      float lsum = iteration(s_cur, s_nxt, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES),
+                             pw_cur, pw_prev, kv_next_k, kv_next_v, kslot(u), vslot(u), active);
+      // the check of tile t before any MFMA uses its probabilities (NaN-safe)
+      const bool raise = !(lsum <= kSumMax) || (m_run == kNegInf && active);
+      if (__builtin_expect(__ballot(raise) != 0, 0)) lsum = raise_reference(s_cur, pw_cur);
+      l_run += lsum;
       // scalars of the next iteration, complete before the barrier so no
       // scalar load is outstanding while the next iteration's LDS reads are
       // counted
       kv_next_k = tile_kv0(t + 1 + STAGES);
-      kv_next_v = tile_kv0(t + STAGES);
+      kv_next_v = tile_kv0(t + STAGES - 1);
       kv_cur = tile_kv0(t + 1);
       bits_cur = mbits ? mbits[t + 1 < nkv_tiles ? t + 1 : nkv_tiles - 1] : full;
       asm volatile("" ::"s"(kv_next_k), "s"(kv_next_v), "s"(kv_cur), "s"(bits_cur));
@@ -549,6 +523,21 @@ void attn_fwd_kernel(AttnArgs a) {
       block_sync();
     }
   }
+  if (nkv_tiles > 0) {
+    // O += P V of the last tile n-1: its V sits in slot (n+1) % STAGES
+    const u32x4* pw_last = ((nkv_tiles - 1) % 2 == 0) ? pwA : pwB;
+    const int sl = (nkv_tiles + 1) % STAGES;
+    const uint8_t* vs_last = vslot(sl);
+    bf16x8 vop[2];
+    vop[0] = load_op(kNA, nullptr, vs_last);
+#pragma unroll
+    for (int j = 0; j < kNB; ++j) {
+      if (j + 1 < kNB) vop[(j + 1) % 2] = load_op(kNA + j + 1, nullptr, vs_last);
+      o[j % 4] = mfma32(vop[j % 2], __builtin_bit_cast(bf16x8, pw_last[j / 4]), o[j % 4]);
+    }
+  }
+  // no load of this workgroup may still be writing LDS when it ends
+  wait_vm_lgkm<0>();
 
   // ---- epilogue
   const float l_tot = l_run + other_half(l_run);

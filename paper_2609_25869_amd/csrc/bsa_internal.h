@@ -115,4 +115,5 @@ hipError_t launch_attention(int tq, int tkv, const AttnArgs& a, hipStream_t s);
 bool attention_variant_exists(int tq, int tkv);
 hipError_t launch_splitk_merge(int tq, const AttnArgs& a, hipStream_t s);
 
+
 }  // namespace bsa

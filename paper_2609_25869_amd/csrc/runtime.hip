@@ -190,6 +190,7 @@ struct bsa_plan_s {
   hipEvent_t ready = nullptr, done = nullptr;
   // device
   uint16_t* zero_page = nullptr;
+
   HeadDesc* heads_dev = nullptr;
   int64_t* row_base_dev = nullptr;
   int32_t* seg_heads_dev = nullptr;

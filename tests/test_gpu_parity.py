@@ -140,6 +140,40 @@ def test_kv_block_permutation_invariance():
         p2.destroy()
 
 
+def _scale_rows(q_bits, factors):
+    """Q rows multiplied by per-row factors (exactly representable scalings of bf16 values)."""
+    from workloads import f32_from_bf16_bits
+    q = f32_from_bf16_bits(q_bits) * factors
+    return bf16_bits_from_f32(q.astype(np.float32))
+
+
+@pytest.mark.parametrize("name", ["g64_ragged", "asym_heads", "g16"])
+@pytest.mark.parametrize("mode", ["all_large", "mixed", "extreme"])
+def test_large_scores_use_the_running_maximum(name, mode):
+    """Scores beyond the fixed-reference bound (scale |q| max|k| > 32 in log2
+    units) take the running-maximum path; wavefronts of one task may take
+    different paths.  Every eligible plan must still match the oracle."""
+    q, k, v, mask = _case(name)
+    B, Nq, H, d = q.shape
+    rng = np.random.default_rng(5)
+    if mode == "all_large":
+        f = np.full((B, Nq, H, 1), 6.0, dtype=np.float32)       # bounds ~100: running maximum
+    elif mode == "mixed":
+        # alternate 32-row groups (one wavefront each): bounded and running-maximum paths in one task
+        grp = (np.arange(Nq) // 32) % 2 == 0
+        f = np.where(grp[None, :, None, None], 8.0, 1.0).astype(np.float32) * np.ones((B, 1, H, 1), np.float32)
+    else:
+        f = np.full((B, Nq, H, 1), 64.0, dtype=np.float32)      # scores in the hundreds
+    q = _scale_rows(q, f)
+    O_ref, L_ref = oattn.masked_attention(q, k, v, mask)
+    for pid in _eligible_plans(mask):
+        log("case %s mode %s plan %d" % (name, mode, pid))
+        p, od, lsed, _ = run_plan(bsa, mask, q, k, v, force_plan=pid)
+        compare(bf16_to_f64(od), O_ref, "%s %s plan %d" % (name, mode, pid))
+        compare_lse(lsed.cpu().numpy().astype(np.float64), L_ref, "%s %s plan %d" % (name, mode, pid))
+        p.destroy()
+
+
 def test_rows_are_convex_combinations_of_allowed_values():
     q, k, v, mask = random_case(503, 1, 2, 384, 384, 128, [(32, 32)] * 2, 0.2, empty_rows=1)
     p, od, _, _ = run_plan(bsa, mask, q, k, v)
