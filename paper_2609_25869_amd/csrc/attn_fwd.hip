@@ -1,24 +1,28 @@
 // Block-sparse attention forward for gfx950 (CDNA4): one workgroup per task,
-// NWAVES wavefronts of 32 query rows each (T_Q = 32 * NWAVES), K/V tiles of
-// TKV tokens streamed through LDS rings of STAGES slots (pipeline depth,
-// Sections 2.3, 4.2, 4.3).  The loop is software pipelined: the scores of
-// tile t+1 (MFMA) are computed while the probabilities of tile t (VALU) are
-// formed and O accumulates P V of tile t-1, whose probabilities were
-// checked at the end of the previous iteration.
+// NWAVES wavefronts, each owning G groups of 32 query rows
+// (T_Q = 32 * G * NWAVES), K/V tiles of TKV tokens streamed through LDS rings
+// of STAGES slots (pipeline depth, Sections 2.3, 4.2, 4.3).  The loop is
+// software pipelined: the scores of tile t+1 (MFMA) are computed while the
+// probabilities of tile t (VALU) are formed and O accumulates P V of tile
+// t-1, whose probabilities were checked at the end of the previous
+// iteration.
 //
 // Layout of the work inside a wavefront
 //   The score tile is computed transposed, S^T = K Q^T, with
-//   v_mfma_f32_32x32x16_bf16 (A = K rows from LDS, B = the wave's Q rows held
-//   in registers).  In the MFMA result each lane owns one query row
-//   (lane % 32) and 16 keys per 32-key block, so the row max needs one
-//   exchange between the two lane halves and the online-softmax state
-//   (running max m, partial sum l) is per lane.  The output is accumulated
-//   transposed as well, O^T += V^T P^T: the B operand is the lane's own
-//   probabilities (no data movement, the key order inside an MFMA is chosen
-//   to match the S^T layout) and the A operand is read from the row-major V
-//   tile with ds_read_b64_tr_b16, which hands each lane 4 keys of one
-//   head-dim column.  Rescaling O by exp2(m_old - m_new) is therefore a
-//   per-lane multiply.
+//   v_mfma_f32_32x32x16_bf16 (A = K rows from LDS, B = a 32-row group of the
+//   wave's Q rows held in registers).  In the MFMA result each lane owns one
+//   query row (lane % 32) of the group and 16 keys per 32-key block, so the
+//   row max needs one exchange between the two lane halves and the
+//   online-softmax state (running max m, partial sum l) is per lane and
+//   group.  The output is accumulated transposed as well, O^T += V^T P^T: the
+//   B operand is the lane's own probabilities (no data movement, the key
+//   order inside an MFMA is chosen to match the S^T layout) and the A operand
+//   is read from the row-major V tile with ds_read_b64_tr_b16, which hands
+//   each lane 4 keys of one head-dim column.  Rescaling O by
+//   exp2(m_old - m_new) is therefore a per-lane multiply.
+//   Every A operand read from LDS feeds G MFMAs, one per row group: with
+//   G = 2 a wave holds 64 query rows, which halves the LDS reads and the K/V
+//   traffic per flop (the register file then holds one wave per SIMD).
 //
 // LDS layout
 //   K and V tiles arrive by direct global->LDS loads (no register staging)
@@ -32,13 +36,14 @@
 // log2(e)/sqrt(d) in fp32 so exp2 is used.  The running reference m of a
 // row is not tracked tile by tile: the probabilities of a tile are formed
 // against the current reference and their sum is checked before any MFMA
-// consumes them; only when a probability may exceed 2^kTau (or the row has
-// no reference yet) is the tile's row maximum formed, the reference raised
-// and O rescaled.  P is rounded to bf16 for the PV product; O is normalised
-// in fp32 and rounded to bf16 (RNE).  Masked entries (outside the tile's
-// active members, or beyond the sequence end) are -inf before any of this;
-// a row whose reference is still unset uses 0 as its reference, so no NaN
-// can arise (it keeps l = 0 and O = 0).
+// consumes them; only when a probability may exceed 2^8 (or the row has
+// no reference yet) is the tile's row maximum formed, the row's reference
+// raised and its O rescaled.  That decision is taken per query row, from the
+// row's own active scores.  P is rounded to bf16 for the PV product; O is
+// normalised in fp32 and rounded to bf16 (RNE).  Masked entries (outside
+// the tile's active members, or beyond the sequence end) are -inf before
+// any of this; a row whose reference is still unset uses 0 as its
+// reference, so no NaN can arise (it keeps l = 0 and O = 0).
 #include "bsa_internal.h"
 
 namespace bsa {
@@ -65,16 +70,50 @@ __device__ inline f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// The same MFMA with the accumulator pinned to VGPRs and B read from AGPRs.
+// Once a kernel needs more than 256 registers the compiler selects the AGPR
+// form for every MFMA; score tiles are VALU operands, and from AGPRs each
+// element would first need a copy.  The hardware does not interlock an MFMA
+// result read by a VALU instruction, nor a VALU-written operand read by an
+// MFMA, and the compiler inserts no wait states around inline assembly, so
+// the callers keep those distances: the next MFMA of the same chain issues
+// at least one other MFMA later, VALU reads of the scores follow a whole
+// pipeline iteration later, and the two places where that does not hold by
+// construction (the Q operands just written, the first tile's scores just
+// computed) get an explicit wait (hazard_wait).
+__device__ inline void mfma32_vacc(f32x16& acc, bf16x8 a, bf16x8 b, bool zero) {
+  if (zero) {
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "a"(b));
+  } else {
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "a"(b));
+  }
+}
+
+// 24 wait states, tied to the registers they protect (the compiler can then
+// move no producer after it and no consumer before it): more than an 8-pass
+// MFMA result needs before a VALU read, and than a VALU write needs before an
+// MFMA reads it.
+template <typename T>
+__device__ inline void hazard_wait_v(T& x) { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(x)); }
+// the same for the Q operands of a 64-row wave, all in one wait
+__device__ inline void hazard_wait_q2(bf16x8 (&q)[2][8]) {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"
+               : "+a"(q[0][0]), "+a"(q[0][1]), "+a"(q[0][2]), "+a"(q[0][3]), "+a"(q[0][4]), "+a"(q[0][5]),
+                 "+a"(q[0][6]), "+a"(q[0][7]), "+a"(q[1][0]), "+a"(q[1][1]), "+a"(q[1][2]), "+a"(q[1][3]),
+                 "+a"(q[1][4]), "+a"(q[1][5]), "+a"(q[1][6]), "+a"(q[1][7]));
+}
+
 __device__ inline i16x4 lds_read_tr(const uint8_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
 }
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-template <int NWAVES, int TKV>
+template <int NWAVES, int G, int TKV>
 struct Cfg {
   static constexpr int kThreads = 64 * NWAVES;
-  static constexpr int kTQ = 32 * NWAVES;
+  static constexpr int kRowsPerWave = 32 * G;
+  static constexpr int kTQ = kRowsPerWave * NWAVES;
   static constexpr int kNKB = TKV / 32;                 // 32-key blocks per tile
   static constexpr int kTileBytes = TKV * kRowBytes;
 };
@@ -90,22 +129,30 @@ __device__ inline int64_t task_of_slot(int64_t slot, int64_t nt) {
 }
 
 // Value of the same register in lane l ^ 32 (the other half of the wave).
-__device__ inline float other_half(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+__device__ inline uint32_t other_half_u32(uint32_t x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
   // lanes 0-31 find the partner in r[1], lanes 32-63 in r[0]; the other entry is x itself
-  return (threadIdx.x & 32) ? __uint_as_float(r[0]) : __uint_as_float(r[1]);
+  return (threadIdx.x & 32) ? r[0] : r[1];
 }
+__device__ inline float other_half(float x) { return __uint_as_float(other_half_u32(__float_as_uint(x))); }
 
 // In-place updates for the rare paths (rescale, masking).  The tied
 // operands pin each result to the register it came from; written as plain
 // C++ the compiler gives the updated values new registers and then copies
 // the whole accumulator on the common path where the update did not run.
+// With G = 2 the accumulators live in AGPRs, which VALU instructions cannot
+// address, and the multiply is left to the compiler.
+template <bool kInVgpr>
 __device__ inline void scale_inplace(f32x16& v, float alpha) {
+  if constexpr (kInVgpr) {
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    float x = v[i];
-    asm volatile("v_mul_f32_e32 %0, %1, %0" : "+v"(x) : "v"(alpha));
-    v[i] = x;
+    for (int i = 0; i < 16; ++i) {
+      float x = v[i];
+      asm volatile("v_mul_f32_e32 %0, %1, %0" : "+v"(x) : "v"(alpha));
+      v[i] = x;
+    }
+  } else {
+    v *= alpha;
   }
 }
 
@@ -115,12 +162,11 @@ __device__ inline void mask_inplace(float& x, bool keep) {
   asm volatile("v_cndmask_b32_e64 %0, %1, %0, %2" : "+v"(x) : "v"(ninf), "s"(__ballot(keep)));
 }
 
-// The reference of a row is only raised when the probabilities of a tile,
-// formed against it, sum to more than 2^kTau in one lane; below that every
-// probability is at most 2^kTau, which fp32 sums and bf16 P hold exactly as
+// A row's reference is raised only when the probabilities of a tile, formed
+// against it, sum to more than 2^8 in one lane; below that every
+// probability is at most 2^8, which fp32 sums and bf16 P hold exactly as
 // well, and the rescale of O is skipped.
-constexpr float kTau = 8.0f;
-constexpr float kSumMax = 256.0f;  // 2^kTau
+constexpr float kSumMax = 256.0f;
 
 // Wait until at most N of this wave's vector-memory operations (the LDS DMA
 // of younger tiles) are outstanding and all of its LDS reads have retired
@@ -142,12 +188,19 @@ __device__ inline void block_sync() {
   asm volatile("" ::: "memory");
 }
 
-template <int NWAVES, int TKV, int STAGES>
-__global__ __launch_bounds__(64 * NWAVES) __attribute__((amdgpu_waves_per_eu(2, 2)))
+// Waves per SIMD the register budget is sized for: two for G = 1, one for
+// G = 2 (its accumulators and Q fragments need the whole register file).
+template <int G>
+constexpr int waves_per_simd() { return G == 1 ? 2 : 1; }
+
+template <int NWAVES, int G, int TKV, int STAGES>
+__global__ __launch_bounds__(64 * NWAVES) __attribute__((amdgpu_waves_per_eu(waves_per_simd<G>(),
+                                                                               waves_per_simd<G>())))
 void attn_fwd_kernel(AttnArgs a) {
-  using C = Cfg<NWAVES, TKV>;
+  using C = Cfg<NWAVES, G, TKV>;
   constexpr int kNKB = C::kNKB;
-  static_assert(STAGES == 2 || STAGES == 4, "ring depth");
+  static_assert(STAGES == 2 || STAGES == 4 || STAGES == 8, "ring depth");
+  static_assert(G == 1 || G == 2, "row groups per wave");
   // A ring of STAGES slots; slot j holds K of a tile x = j (mod STAGES) and
   // V of tile x-2.  Iteration t reads slot (t+1) % STAGES: K of tile t+1
   // (scores of the next tile) and V of tile t-1 (O += P V of the previous
@@ -157,12 +210,28 @@ void attn_fwd_kernel(AttnArgs a) {
   // sees that reads of one slot never alias the DMA filling another and
   // keeps those loads in flight.
   constexpr int kSlotBytes = 2 * C::kTileBytes;
-  constexpr int kSpareBytes = STAGES > 2 ? kSlotBytes : 16;
+  constexpr int kBytes4 = STAGES > 2 ? kSlotBytes : 16;   // slots 2-3
+  constexpr int kBytes8 = STAGES > 4 ? kSlotBytes : 16;   // slots 4-7
   __shared__ __attribute__((aligned(1024))) uint8_t ring0[kSlotBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t ring1[kSlotBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t ring2[kSpareBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t ring3[kSpareBytes];
-  auto kslot = [&](int i) -> uint8_t* { return i == 0 ? ring0 : i == 1 ? ring1 : i == 2 ? ring2 : ring3; };
+  __shared__ __attribute__((aligned(1024))) uint8_t ring2[kBytes4];
+  __shared__ __attribute__((aligned(1024))) uint8_t ring3[kBytes4];
+  __shared__ __attribute__((aligned(1024))) uint8_t ring4[kBytes8];
+  __shared__ __attribute__((aligned(1024))) uint8_t ring5[kBytes8];
+  __shared__ __attribute__((aligned(1024))) uint8_t ring6[kBytes8];
+  __shared__ __attribute__((aligned(1024))) uint8_t ring7[kBytes8];
+  auto kslot = [&](int i) -> uint8_t* {
+    switch (i) {
+      case 0: return ring0;
+      case 1: return ring1;
+      case 2: return ring2;
+      case 3: return ring3;
+      case 4: return ring4;
+      case 5: return ring5;
+      case 6: return ring6;
+      default: return ring7;
+    }
+  };
   auto vslot = [&](int i) -> uint8_t* { return kslot(i) + C::kTileBytes; };
 
   const int64_t nt = a.ntasks_dev ? *a.ntasks_dev : a.ntasks;
@@ -173,22 +242,27 @@ void attn_fwd_kernel(AttnArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
-  const int n = lane & 31;   // query row of this lane inside the wave
+  const int n = lane & 31;   // query row of this lane inside a 32-row group
   const int hh = lane >> 5;  // lane half
   const int b = task.bh / a.H, h = task.bh - b * a.H;
   const int q0 = task.pq * C::kTQ;
-  const int qrow = q0 + 32 * w + n;
+  // row of group g inside the task's query tile, and in the sequence
+  auto q_local = [&](int g) { return C::kRowsPerWave * w + 32 * g + n; };
+  auto q_row = [&](int g) { return q0 + q_local(g); };
 
-  // ---- Q fragment: B operand of S^T = K Q^T, lane (n, hh) holds d = 16c + 8hh .. +8
+  // ---- Q fragments: B operands of S^T = K Q^T, lane (n, hh) of group g
+  // holds d = 16c + 8hh .. +8 of its row
   const float c_log2 = a.scale_log2;
-  bf16x8 qf[8];
-  {
-    const uint16_t* qp = a.q + b * a.qs0 + h * a.qs1 + (int64_t)(qrow < a.Nq ? qrow : 0) * a.qs2;
+  bf16x8 qf[G][8];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) qf[c] = *reinterpret_cast<const bf16x8*>(qp + 16 * c + 8 * hh);
-    if (qrow >= a.Nq) {
+  for (int g = 0; g < G; ++g) {
+    const int qr = q_row(g);
+    const uint16_t* qp = a.q + b * a.qs0 + h * a.qs1 + (int64_t)(qr < a.Nq ? qr : 0) * a.qs2;
 #pragma unroll
-      for (int c = 0; c < 8; ++c) qf[c] = bf16x8{};
+    for (int c = 0; c < 8; ++c) qf[g][c] = *reinterpret_cast<const bf16x8*>(qp + 16 * c + 8 * hh);
+    if (qr >= a.Nq) {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) qf[g][c] = bf16x8{};
     }
   }
 
@@ -259,7 +333,7 @@ void attn_fwd_kernel(AttnArgs a) {
   for (int c = 0; c < 8; ++c) koff[c] = (lane & 31) * kRowBytes + (((2 * c + hh) ^ sw) << 4);
   int voff[2][4];  // V transposed read: [r][dblk]
   {
-    const int s16 = lane & 15, g = lane >> 4, mh = g & 1, gh = g >> 1;
+    const int s16 = lane & 15, gi = lane >> 4, mh = gi & 1, gh = gi >> 1;
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
       const int row = 8 * r + 4 * gh + (s16 >> 2);  // within a 16-key chunk
@@ -271,21 +345,31 @@ void attn_fwd_kernel(AttnArgs a) {
     }
   }
 
-  // membership decode for this lane's query row
-  const int q_local = 32 * w + n;
-  const int mem_row = (a.gq > 1) ? (q_local >> a.bq_shift) : 0;
+  // membership decode for this lane's query rows
+  int mem_row[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) mem_row[g] = (a.gq > 1) ? (q_local(g) >> a.bq_shift) : 0;
   const int mem_bits = a.gq * a.gkv;
   const uint64_t full = (mem_bits >= 64) ? ~0ull : ((1ull << mem_bits) - 1);
   const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-  f32x16 o[4];
+  f32x16 o[G][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) o[i] = f32x16{};
-  float m_run = kNegInf, l_run = 0.f;
+  for (int g = 0; g < G; ++g) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[g][i] = f32x16{};
+  }
+  float m_run[G], l_run[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m_run[g] = kNegInf;
+    l_run[g] = 0.f;
+  }
 
   // MFMA operand stream of one iteration: units [0, kNA) are the S^T MFMAs of
   // the next tile (A = K rows), units [kNA, kNU) the O^T MFMAs of this tile
-  // (A = V^T via transposed reads).  Operands are read two units ahead.
+  // (A = V^T via transposed reads); each unit issues one MFMA per row group
+  // with the same A operand.  Operands are read kAhead units ahead.
   constexpr int kNA = 8 * kNKB;
   constexpr int kNB = 4 * (TKV / 16);
   constexpr int kNU = kNA + kNB;
@@ -300,24 +384,33 @@ void attn_fwd_kernel(AttnArgs a) {
     return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   };
 
+  // Score and probability registers of one tile are indexed [g * kNKB + kb]
+  // (score blocks) and [g * kChunks + c] (packed bf16 P chunks).
+  constexpr int kE = 16 * kNKB;           // score elements per lane and group
+  constexpr int kChunks = TKV / 16;       // 8-element P chunks per group
+
   // raw scores S^T of one tile with nothing else to overlap (prologue)
   auto qk_only = [&](const uint8_t* ks, f32x16* s) {
 #pragma unroll
-    for (int kb = 0; kb < kNKB; ++kb) s[kb] = f32x16{};
+    for (int i = 0; i < G * kNKB; ++i) s[i] = f32x16{};
     bf16x8 op[3];
     op[0] = load_op(0, ks, nullptr);
     op[1] = load_op(1, ks, nullptr);
 #pragma unroll
     for (int u = 0; u < kNA; ++u) {
       if (u + 2 < kNA) op[(u + 2) % 3] = load_op(u + 2, ks, nullptr);
-      s[u % kNKB] = mfma32(op[u % 3], qf[u / kNKB], s[u % kNKB]);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        if constexpr (G == 1) s[g * kNKB + u % kNKB] = mfma32(op[u % 3], qf[g][u / kNKB], s[g * kNKB + u % kNKB]);
+        else mfma32_vacc(s[g * kNKB + u % kNKB], op[u % 3], qf[g][u / kNKB], u < kNKB);
+      }
     }
   };
 
   // entries outside the tile's active members or past the sequence end ->
   // -inf; returns whether this lane's row keeps any key of the tile
-  auto apply_mask = [&](f32x16* s, int kv0, uint64_t bits) -> bool {
-    const uint64_t rowbits = bits >> (mem_row * a.gkv);
+  auto apply_mask = [&](f32x16* s, int kv0, uint64_t bits, int mrow) -> bool {
+    const uint64_t rowbits = bits >> (mrow * a.gkv);
     // allowed-key bitmap of this lane's row over the tile
     uint64_t allowed = 0;
     const int nvalid = min(TKV, a.Nkv - kv0);
@@ -345,8 +438,8 @@ void attn_fwd_kernel(AttnArgs a) {
     return allowed != 0;
   };
 
-  // Row maximum of one tile's raw scores (the scale is positive), both lane
-  // halves combined.
+  // Row maximum of one group's raw scores in a tile (the scale is positive),
+  // both lane halves combined.
   auto row_max = [&](const f32x16* s) -> float {
     float mx = kNegInf;
 #pragma unroll
@@ -357,19 +450,19 @@ void attn_fwd_kernel(AttnArgs a) {
     return fmaxf(mx, other_half(mx));
   };
 
-  // Distribution of the VALU work of one iteration over its MFMA units.
-  // A probability is made in two steps one unit apart: the exponential
+  // Distribution of the VALU work of one iteration over its MFMAs.
+  // A probability is made in two steps one slot apart: the exponential
   // (stage A) and, for a pair of them, the bf16 packing and the row-sum dot
-  // product (stage B), so no unit waits on an exponential it just issued.
-  // Stage A is spread over all but the last unit; none of it feeds an MFMA
+  // product (stage B), so no slot waits on an exponential it just issued.
+  // Stage A is spread over all but the last slot; none of it feeds an MFMA
   // of the same iteration.
-  constexpr int kE = 16 * kNKB;           // score elements per lane
-  constexpr int kChunks = TKV / 16;       // 8-element P chunks
+  constexpr int kEAll = G * kE;           // score elements per lane, all groups
   constexpr int kGroupLoads = 2 * kLoadsPerWave;  // refill loads of one iteration
   constexpr int kDmaEvery = kNU / kGroupLoads;
   static_assert(kDmaEvery >= 1 && kDmaEvery * kGroupLoads <= kNU, "refill loads must fit the units");
-  // elements whose exponential is formed by the end of unit uu
-  auto a_end = [&](int uu) -> int { return uu < 0 ? 0 : uu < kNU - 1 ? (uu + 1) * kE / (kNU - 1) : kE; };
+  constexpr int kNS = kNU * G;            // MFMA slots of one iteration
+  // elements whose exponential is formed by the end of slot ss
+  auto a_end = [&](int ss) -> int { return ss < 0 ? 0 : ss < kNS - 1 ? (ss + 1) * kEAll / (kNS - 1) : kEAll; };
   constexpr int kAhead = 3;  // operand read distance, in units
 
   // probability of a raw score against the reference -nm, and the bf16
@@ -381,25 +474,36 @@ void attn_fwd_kernel(AttnArgs a) {
   // One pipeline iteration over tile t: (rare) masking of s_cur; the S^T
   // MFMAs of tile t+1 (K from ks_next) and the O^T MFMAs of tile t-1 (V from
   // vs_prev, P from pw_prev) interleaved with the probabilities of tile t
-  // (into pw_cur).  Returns the lane's sum of those probabilities; active
-  // tells whether the lane's row has a key in tile t.
+  // (into pw_cur).  Leaves each group's lane sum of those probabilities in
+  // lsum; active tells whether the lane's row of a group has a key in tile t.
   auto iteration = [&](f32x16* s_cur, f32x16* s_nxt, int kv0_cur, uint64_t bits_cur, const uint8_t* ks_next,
                        const uint8_t* vs_prev, u32x4* pw_cur, const u32x4* pw_prev, int kv0_refill_k,
-                       int kv0_refill_v, uint8_t* k_refill, uint8_t* v_refill, bool& active) -> float {
+                       int kv0_refill_v, uint8_t* k_refill, uint8_t* v_refill, bool* active, float* lsum) {
     // the ring refill of this iteration, one load every kDmaEvery units
     const __amdgpu_buffer_rsrc_t rk = tile_rsrc(kbase, kstride, kv0_refill_k);
     const __amdgpu_buffer_rsrc_t rv = tile_rsrc(vbase, vstride, kv0_refill_v);
-    active = true;
-    if (__builtin_expect(kv0_cur + TKV > a.Nkv || bits_cur != full, 0)) active = apply_mask(s_cur, kv0_cur, bits_cur);
-    const float nm = (m_run == kNegInf) ? 0.f : -m_run;
-    float ls0 = 0.f, ls1 = 0.f;
-    float pf[kE];
-    auto stage_a = [&](int ei) { pf[ei] = exponent(s_cur[ei / 16][ei % 16], nm); };
+#pragma unroll
+    for (int g = 0; g < G; ++g) active[g] = true;
+    if (__builtin_expect(kv0_cur + TKV > a.Nkv || bits_cur != full, 0)) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) active[g] = apply_mask(s_cur + g * kNKB, kv0_cur, bits_cur, mem_row[g]);
+    }
+    float nm[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) nm[g] = (m_run[g] == kNegInf) ? 0.f : -m_run[g];
+    float ls[G][2];
+#pragma unroll
+    for (int g = 0; g < G; ++g) ls[g][0] = ls[g][1] = 0.f;
+    float pf[kEAll];
+    auto stage_a = [&](int ei) {
+      const int g = ei / kE, e = ei % kE;
+      pf[ei] = exponent(s_cur[g * kNKB + e / 16][e % 16], nm[g]);
+    };
     auto stage_b = [&](int pr) {
-      const int e0 = 2 * pr;
+      const int e0 = 2 * pr, g = e0 / kE, el = e0 % kE;
       const bf16x2 pair = pack_pair(pf[e0], pf[e0 + 1]);
-      pw_cur[e0 / 8][(e0 % 8) / 2] = __builtin_bit_cast(uint32_t, pair);
-      float& acc = (pr & 1) ? ls1 : ls0;
+      pw_cur[g * kChunks + el / 8][(el % 8) / 2] = __builtin_bit_cast(uint32_t, pair);
+      float& acc = ls[g][pr & 1];
       acc = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, acc, false);
       // keep the sum in this unit (otherwise it is sunk to the end of the loop)
       asm volatile("" : "+v"(acc));
@@ -407,63 +511,78 @@ void attn_fwd_kernel(AttnArgs a) {
     bf16x8 op[kAhead + 1];
 #pragma unroll
     for (int u = 0; u < kAhead; ++u) op[u] = load_op(u, ks_next, vs_prev);
+    // one MFMA per slot: slot sl is row group sl % G of unit sl / G, so the
+    // VALU work between two MFMAs of the wave stays short
 #pragma unroll
-    for (int u = 0; u < kNU; ++u) {
-      if (u + kAhead < kNU) op[(u + kAhead) % (kAhead + 1)] = load_op(u + kAhead, ks_next, vs_prev);
-      if (u % kDmaEvery == 0 && u / kDmaEvery < kGroupLoads) {
-        const int i = u / kDmaEvery;
-        if (i < kLoadsPerWave) dma_one(rk, kstride, koffs, i, k_refill);
-        else dma_one(rv, vstride, voffs, i - kLoadsPerWave, v_refill);
+    for (int sl = 0; sl < kNS; ++sl) {
+      const int u = sl / G, g = sl % G;
+      if (g == 0) {
+        if (u + kAhead < kNU) op[(u + kAhead) % (kAhead + 1)] = load_op(u + kAhead, ks_next, vs_prev);
+        if (u % kDmaEvery == 0 && u / kDmaEvery < kGroupLoads) {
+          const int i = u / kDmaEvery;
+          if (i < kLoadsPerWave) dma_one(rk, kstride, koffs, i, k_refill);
+          else dma_one(rv, vstride, voffs, i - kLoadsPerWave, v_refill);
+        }
       }
       if (u < kNA) {
-        s_nxt[u % kNKB] = mfma32(op[u % (kAhead + 1)], qf[u / kNKB], u < kNKB ? f32x16{} : s_nxt[u % kNKB]);
+        f32x16& acc = s_nxt[g * kNKB + u % kNKB];
+        if constexpr (G == 1) {
+          acc = mfma32(op[u % (kAhead + 1)], qf[g][u / kNKB], u < kNKB ? f32x16{} : acc);
+        } else {
+          mfma32_vacc(acc, op[u % (kAhead + 1)], qf[g][u / kNKB], u < kNKB);
+        }
       } else {
         const int j = u - kNA;
-        o[j % 4] = mfma32(op[u % (kAhead + 1)], __builtin_bit_cast(bf16x8, pw_prev[j / 4]), o[j % 4]);
+        o[g][j % 4] = mfma32(op[u % (kAhead + 1)], __builtin_bit_cast(bf16x8, pw_prev[g * kChunks + j / 4]),
+                             o[g][j % 4]);
       }
 #pragma unroll
-      for (int pr = a_end(u - 2) / 2; pr < a_end(u - 1) / 2; ++pr) stage_b(pr);
+      for (int pr = a_end(sl - 2) / 2; pr < a_end(sl - 1) / 2; ++pr) stage_b(pr);
 #pragma unroll
-      for (int e = a_end(u - 1); e < a_end(u); ++e) stage_a(e);
+      for (int e = a_end(sl - 1); e < a_end(sl); ++e) stage_a(e);
       __builtin_amdgcn_sched_barrier(0);
     }
-    return ls0 + ls1;
+#pragma unroll
+    for (int g = 0; g < G; ++g) lsum[g] = ls[g][0] + ls[g][1];
   };
 
-  // Rare path after an iteration: a probability of tile t may exceed 2^kTau
-  // (or some row met its first key).  Raise each row's reference to the
-  // maximum of its scores so far, rescale O and l, and form the tile's
-  // probabilities again.  O holds P V up to tile t-1, all against the old
-  // reference, so one factor per row covers it.
-  auto raise_reference = [&](const f32x16* s_cur, u32x4* pw_cur) -> float {
-    const float mxs = row_max(s_cur) * c_log2;
-    const float m_new = fmaxf(m_run, mxs);
-    const float alpha = (m_new == m_run) ? 1.f : fast_exp2(m_run - m_new);
-    m_run = m_new;
-    l_run *= alpha;
+  // Rare path after an iteration, for row group g: in the rows flagged by
+  // `mine` (both lane halves of a row agree) a probability of tile t may
+  // exceed 2^8, or the row met its first key.  Raise those rows' reference
+  // to the maximum of their scores so far, rescale their O and l, and form
+  // the tile's probabilities again.  O holds P V up to tile t-1, all against
+  // the old reference, so one factor per row covers it.  Other rows keep
+  // their state exactly: their factor is 1 and their probabilities are
+  // formed again from the same operands, which gives the same bits.
+  auto raise_reference = [&](int g, const f32x16* s_cur, u32x4* pw_cur, bool mine, float lsum_old) -> float {
+    const float mxs = row_max(s_cur + g * kNKB) * c_log2;
+    const float m_new = mine ? fmaxf(m_run[g], mxs) : m_run[g];
+    const float alpha = (m_new == m_run[g]) ? 1.f : fast_exp2(m_run[g] - m_new);
+    m_run[g] = m_new;
+    l_run[g] *= alpha;
 #pragma unroll
-    for (int d = 0; d < 4; ++d) scale_inplace(o[d], alpha);
-    const float nm = (m_run == kNegInf) ? 0.f : -m_run;
+    for (int d = 0; d < 4; ++d) scale_inplace<G == 1>(o[g][d], alpha);
+    const float nm = (m_run[g] == kNegInf) ? 0.f : -m_run[g];
     float ls = 0.f;
 #pragma unroll
     for (int pr = 0; pr < kE / 2; ++pr) {
       const int e0 = 2 * pr;
-      const bf16x2 pair =
-          pack_pair(exponent(s_cur[e0 / 16][e0 % 16], nm), exponent(s_cur[e0 / 16][e0 % 16 + 1], nm));
-      pw_cur[e0 / 8][(e0 % 8) / 2] = __builtin_bit_cast(uint32_t, pair);
+      const bf16x2 pair = pack_pair(exponent(s_cur[g * kNKB + e0 / 16][e0 % 16], nm),
+                                    exponent(s_cur[g * kNKB + e0 / 16][e0 % 16 + 1], nm));
+      pw_cur[g * kChunks + e0 / 8][(e0 % 8) / 2] = __builtin_bit_cast(uint32_t, pair);
       ls = __builtin_amdgcn_fdot2_f32_bf16(pair, ones2, ls, false);
     }
-    return ls;
+    return mine ? ls : lsum_old;
   };
 
   // number of DMA instructions one iteration issues (K tile and V tile)
   constexpr int kGroup = 2 * kLoadsPerWave;
   constexpr int kInFlight = (STAGES - 2) * kGroup;
 
-  f32x16 sA[kNKB], sB[kNKB];
-  u32x4 pwA[kChunks], pwB[kChunks];
+  f32x16 sA[G * kNKB], sB[G * kNKB];
+  u32x4 pwA[G * kChunks], pwB[G * kChunks];
 #pragma unroll
-  for (int c = 0; c < kChunks; ++c) pwB[c] = u32x4{};  // P of "tile -1": no contribution
+  for (int c = 0; c < G * kChunks; ++c) pwB[c] = u32x4{};  // P of "tile -1": no contribution
   // scalars for the coming iteration, fetched one iteration ahead
   int kv_next_k = 0, kv_next_v = 0, kv_cur = 0;
   uint64_t bits_cur = full;
@@ -487,7 +606,12 @@ void attn_fwd_kernel(AttnArgs a) {
     // the scores of tile 0 need K0 only
     wait_vm_lgkm<(STAGES - 1) * kGroup>();
     block_sync();
+    if constexpr (G > 1) hazard_wait_q2(qf);
     qk_only(kslot(0), sA);
+    if constexpr (G > 1) {
+#pragma unroll
+      for (int i = 0; i < G * kNKB; ++i) hazard_wait_v(sA[i]);
+    }
     // the first iteration needs slot 1
     wait_vm_lgkm<kInFlight>();
     block_sync();  // every wave has read slot 0 before it is refilled
@@ -503,13 +627,30 @@ void attn_fwd_kernel(AttnArgs a) {
       f32x16* s_nxt = (u % 2 == 0) ? sB : sA;
       u32x4* pw_cur = (u % 2 == 0) ? pwA : pwB;
       u32x4* pw_prev = (u % 2 == 0) ? pwB : pwA;
-      bool active;
-      float lsum = iteration(s_cur, s_nxt, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES),
-                             pw_cur, pw_prev, kv_next_k, kv_next_v, kslot(u), vslot(u), active);
+      bool active[G];
+      float lsum[G];
+      iteration(s_cur, s_nxt, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES), pw_cur, pw_prev,
+                kv_next_k, kv_next_v, kslot(u), vslot(u), active, lsum);
       // the check of tile t before any MFMA uses its probabilities (NaN-safe)
-      const bool raise = !(lsum <= kSumMax) || (m_run == kNegInf && active);
-      if (__builtin_expect(__ballot(raise) != 0, 0)) lsum = raise_reference(s_cur, pw_cur);
-      l_run += lsum;
+      bool need[G], any = false;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        need[g] = !(lsum[g] <= kSumMax) || (m_run[g] == kNegInf && active[g]);
+        any = any || need[g];
+      }
+      if (__builtin_expect(__ballot(any) != 0, 0)) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          // both lane halves of a row take the same decision; the exchange
+          // runs in every lane (a short-circuit || would run it only where
+          // need is false, and a lane swap there reads inactive partners)
+          const uint32_t mine = need[g] ? 1u : 0u;
+          const bool row = (mine | other_half_u32(mine)) != 0;
+          if (__ballot(row) != 0) lsum[g] = raise_reference(g, s_cur, pw_cur, row, lsum[g]);
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) l_run[g] += lsum[g];
       // scalars of the next iteration, complete before the barrier so no
       // scalar load is outstanding while the next iteration's LDS reads are
       // counted
@@ -533,49 +674,55 @@ void attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
     for (int j = 0; j < kNB; ++j) {
       if (j + 1 < kNB) vop[(j + 1) % 2] = load_op(kNA + j + 1, nullptr, vs_last);
-      o[j % 4] = mfma32(vop[j % 2], __builtin_bit_cast(bf16x8, pw_last[j / 4]), o[j % 4]);
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+        o[g][j % 4] = mfma32(vop[j % 2], __builtin_bit_cast(bf16x8, pw_last[g * kChunks + j / 4]), o[g][j % 4]);
     }
   }
   // no load of this workgroup may still be writing LDS when it ends
   wait_vm_lgkm<0>();
 
   // ---- epilogue
-  const float l_tot = l_run + other_half(l_run);
-  if (task.nsplit == 1) {
-    if (qrow < a.Nq) {
-      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-      uint16_t* op = a.o + b * a.os0 + h * a.os1 + (int64_t)qrow * a.os2;
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const float l_tot = l_run[g] + other_half(l_run[g]);
+    const int ql = q_local(g), qr = q_row(g);
+    if (task.nsplit == 1) {
+      if (qr < a.Nq) {
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        uint16_t* op = a.o + b * a.os0 + h * a.os1 + (int64_t)qr * a.os2;
+#pragma unroll
+        for (int dblk = 0; dblk < 4; ++dblk) {
+#pragma unroll
+          for (int gg = 0; gg < 4; ++gg) {
+            bf16x4 v4;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(o[g][dblk][4 * gg + e] * inv);
+            *reinterpret_cast<bf16x4*>(op + dblk * 32 + 8 * gg + 4 * hh) = v4;
+          }
+        }
+        if (a.lse && hh == 0) {
+          a.lse[((int64_t)b * a.H + h) * a.Nq + qr] =
+              l_tot > 0.f ? (m_run[g] + __log2f(l_tot)) * 0.69314718055994530942f : kNegInf;
+        }
+      }
+    } else {
+      // Split-K partial state: reference m (log2 domain), l, O unnormalised
+      float* slot = a.ws + ti * (int64_t)C::kTQ * (kD + 2);
+      if (hh == 0) {
+        slot[ql] = l_tot > 0.f ? m_run[g] : kNegInf;
+        slot[C::kTQ + ql] = l_tot;
+      }
+      float* os = slot + 2 * C::kTQ + (int64_t)ql * kD;
 #pragma unroll
       for (int dblk = 0; dblk < 4; ++dblk) {
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          bf16x4 v4;
+        for (int gg = 0; gg < 4; ++gg) {
+          f32x4 v4;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(o[dblk][4 * g + e] * inv);
-          *reinterpret_cast<bf16x4*>(op + dblk * 32 + 8 * g + 4 * hh) = v4;
+          for (int e = 0; e < 4; ++e) v4[e] = o[g][dblk][4 * gg + e];
+          *reinterpret_cast<f32x4*>(os + dblk * 32 + 8 * gg + 4 * hh) = v4;
         }
-      }
-      if (a.lse && hh == 0) {
-        a.lse[((int64_t)b * a.H + h) * a.Nq + qrow] =
-            l_tot > 0.f ? (m_run + __log2f(l_tot)) * 0.69314718055994530942f : kNegInf;
-      }
-    }
-  } else {
-    // Split-K partial state: reference m (log2 domain), l, O unnormalised
-    float* slot = a.ws + ti * (int64_t)C::kTQ * (kD + 2);
-    if (hh == 0) {
-      slot[q_local] = l_tot > 0.f ? m_run : kNegInf;
-      slot[C::kTQ + q_local] = l_tot;
-    }
-    float* os = slot + 2 * C::kTQ + (int64_t)q_local * kD;
-#pragma unroll
-    for (int dblk = 0; dblk < 4; ++dblk) {
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        f32x4 v4;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v4[e] = o[dblk][4 * g + e];
-        *reinterpret_cast<f32x4*>(os + dblk * 32 + 8 * g + 4 * hh) = v4;
       }
     }
   }
@@ -631,16 +778,18 @@ __global__ __launch_bounds__(256) void splitk_merge_kernel(AttnArgs a) {
   }
 }
 
-// Ring depth per KV tile: four slots for 32-key tiles, two for 64-key tiles
-// (64 KB of LDS per workgroup either way, so two workgroups share a CU).
-constexpr int stages_for(int tkv) { return tkv == 32 ? 4 : 2; }
+// Ring depth per KV tile: with two waves per SIMD, four slots for 32-key
+// tiles and two for 64-key tiles (64 KB of LDS per workgroup, two
+// workgroups per CU); a 64-row-per-wave workgroup has the CU to itself and
+// takes eight slots (128 KB), so its loads have six iterations to land.
+constexpr int stages_for(int tkv, int g) { return g == 2 ? 8 : tkv == 32 ? 4 : 2; }
 
-template <int NWAVES, int TKV>
+template <int NWAVES, int G, int TKV>
 hipError_t launch_variant(const AttnArgs& a, hipStream_t s) {
   const int64_t slots = ((int64_t)a.ntasks + 7) / 8 * 8;
   if (slots == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_fwd_kernel<NWAVES, TKV, stages_for(TKV)>), dim3((unsigned)slots), dim3(64 * NWAVES), 0,
-                     s, a);
+  hipLaunchKernelGGL((attn_fwd_kernel<NWAVES, G, TKV, stages_for(TKV, G)>), dim3((unsigned)slots),
+                     dim3(64 * NWAVES), 0, s, a);
   return hipGetLastError();
 }
 
@@ -650,13 +799,17 @@ bool attention_variant_exists(int tq, int tkv) {
   return (tq == 64 || tq == 128 || tq == 256) && (tkv == 32 || tkv == 64);
 }
 
+// Kernel per physical tile shape.  T_Q = 256 with 32-key tiles runs four
+// waves of 64 rows (two row groups sharing every K and V operand); with
+// 64-key tiles the two groups' score and probability registers do not fit
+// beside the accumulators, and eight waves of 32 rows run instead.
 hipError_t launch_attention(int tq, int tkv, const AttnArgs& a, hipStream_t s) {
-  if (tq == 64 && tkv == 32) return launch_variant<2, 32>(a, s);
-  if (tq == 64 && tkv == 64) return launch_variant<2, 64>(a, s);
-  if (tq == 128 && tkv == 32) return launch_variant<4, 32>(a, s);
-  if (tq == 128 && tkv == 64) return launch_variant<4, 64>(a, s);
-  if (tq == 256 && tkv == 32) return launch_variant<8, 32>(a, s);
-  if (tq == 256 && tkv == 64) return launch_variant<8, 64>(a, s);
+  if (tq == 64 && tkv == 32) return launch_variant<2, 1, 32>(a, s);
+  if (tq == 64 && tkv == 64) return launch_variant<2, 1, 64>(a, s);
+  if (tq == 128 && tkv == 32) return launch_variant<4, 1, 32>(a, s);
+  if (tq == 128 && tkv == 64) return launch_variant<4, 1, 64>(a, s);
+  if (tq == 256 && tkv == 32) return launch_variant<4, 2, 32>(a, s);
+  if (tq == 256 && tkv == 64) return launch_variant<8, 1, 64>(a, s);
   return hipErrorInvalidValue;
 }
 
