@@ -176,7 +176,9 @@ BSA_API bsa_status bsa_catalog_get(int32_t id, bsa_catalog_entry* out);
 
 /* Eligible(P, R) of Section 4.4 for catalog plan `plan_id`, logical geometry
  * (bq, bkv) and shapes: supported dtype, head dim, layout, tile/block nesting
- * and membership size.  *eligible receives 0 or 1.  Host only. */
+ * and membership size, and one head's K and V rows addressable with 32-bit
+ * byte offsets ((seq_kv + 64) * token stride * 2 + 256 < 4 GiB).  *eligible
+ * receives 0 or 1.  Host only. */
 BSA_API bsa_status bsa_plan_eligible(int32_t plan_id, int32_t bq, int32_t bkv, const bsa_shapes* shapes,
                              int32_t* eligible);
 

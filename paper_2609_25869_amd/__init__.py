@@ -3,7 +3,8 @@
 Python binding of libbsa.so (include/bsa.h).  Torch supplies device memory
 and streams; every step of planning and execution runs in the library's HIP
 kernels.  Importing the package raises ImportError if the library has not
-been built (``python -m paper_2609_25869_amd.build``).
+been built (``python paper_2609_25869_amd/build.py``, a standalone script:
+the package itself cannot be imported before the library exists).
 
     plan = bsa.plan(mask_dev, head_offset, stride_b, B_Q, B_KV, q, k, v, o)
     bsa.forward(plan, q, k, v, o, lse)          # warm repeats reuse the plan

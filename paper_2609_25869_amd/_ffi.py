@@ -89,7 +89,7 @@ def load() -> ctypes.CDLL:
     except ImportError:
         pass
     if not os.path.exists(LIB_PATH):
-        raise ImportError("libbsa.so is not built at %s; run `python -m paper_2609_25869_amd.build`" % LIB_PATH)
+        raise ImportError("libbsa.so is not built at %s; run `python paper_2609_25869_amd/build.py`" % LIB_PATH)
     lib = ctypes.CDLL(LIB_PATH)
     for name, res, args in SIGNATURES:
         fn = getattr(lib, name)

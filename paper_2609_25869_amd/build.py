@@ -1,6 +1,9 @@
 """Build libbsa.so (HIP for gfx950) in-tree with hipcc.
 
-Usage: python -m paper_2609_25869_amd.build [--jobs N]
+Usage: python paper_2609_25869_amd/build.py [--jobs N]
+
+Run it as a script: importing it through the package would import the
+package, which refuses to load before libbsa.so exists.
 """
 from __future__ import annotations
 

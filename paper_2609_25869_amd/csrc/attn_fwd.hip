@@ -274,16 +274,17 @@ void attn_fwd_kernel(AttnArgs a) {
   const int tb = task.tile_begin;
   const int nkv_tiles = task.tile_end - tb;
   ci32p kvt = (ci32p)(a.kv_tile + tb);
-  cu64p mbits = a.member ? (cu64p)(a.member + tb) : nullptr;
 
   // ---- K/V tiles: buffer loads straight into LDS
   // One instruction moves 64 lanes x 16 bytes = 4 token rows into 1 KB of
   // LDS, lane i landing at byte 16 * i.  Lane i of load j owns LDS row
   // rr = 4 * (w + j * NWAVES) + i / 16 and physical chunk i % 16, and reads
-  // the logical chunk that the swizzle places there, at a per-lane byte
-  // offset fixed for the whole task.  Each tile gets a buffer descriptor
-  // whose size covers only the tile's tokens inside the sequence, so rows
-  // past the end read as zero with no extra instruction.
+  // the logical chunk that the swizzle places there.  One buffer descriptor
+  // per tensor covers the head's Nkv tokens, so rows past the sequence end
+  // read as zero with no extra instruction; a load's per-lane byte offset is
+  // the lane's offset inside its row group plus the group's first token times
+  // the token stride, in 32 bits (plan eligibility keeps one head's K/V rows
+  // within 4 GiB).
   constexpr int kLoadsPerWave = TKV / (4 * NWAVES);
   static_assert(kLoadsPerWave >= 1 && TKV % (4 * NWAVES) == 0, "tile rows must split over the waves");
   const char* kbase = reinterpret_cast<const char*>(a.k + b * a.ks0 + h * a.ks1);
@@ -302,27 +303,27 @@ void attn_fwd_kernel(AttnArgs a) {
     koffs[j] = (uint32_t)(rr * kstride) + ch * 16;
     voffs[j] = (uint32_t)(rr * vstride) + ch * 16;
   }
-  // descriptor of the TKV tokens starting at kv0
-  auto tile_rsrc = [&](const char* base, int64_t stride, int kv0) {
-    const int rows = min(TKV, a.Nkv - kv0);
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base + (int64_t)kv0 * stride), 0,
-                                             (int)(rows * stride), 0x00020000);
-  };
-  // load j of this wave's share of one tile
-  auto dma_one = [&](__amdgpu_buffer_rsrc_t rsrc, int64_t stride, const uint32_t* offs, int j, uint8_t* dst_arr) {
-    const int soff = (j / kRep) * (kRep * 4 * NWAVES) * (int)stride;
+  const __amdgpu_buffer_rsrc_t krsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(kbase), 0, (int)((int64_t)a.Nkv * kstride), 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(vbase), 0, (int)((int64_t)a.Nkv * vstride), 0x00020000);
+  // load j of this wave's share of the tile starting at token kv0
+  auto dma_one = [&](__amdgpu_buffer_rsrc_t rsrc, int64_t stride, const uint32_t* offs, int kv0, int j,
+                     uint8_t* dst_arr) {
+    const uint32_t row0 = (uint32_t)(kv0 + (j / kRep) * (kRep * 4 * NWAVES)) * (uint32_t)stride;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        rsrc, (__attribute__((address_space(3))) void*)(dst_arr + 1024 * (w + j * NWAVES)), 16, offs[j % kRep], soff,
-        0, 0);
+        rsrc, (__attribute__((address_space(3))) void*)(dst_arr + 1024 * (w + j * NWAVES)), 16, offs[j % kRep] + row0,
+        0, 0, 0);
   };
   // copy the TKV tokens starting at kv0 into one ring slot
-  auto dma_rows = [&](const char* base, int64_t stride, const uint32_t* offs, int kv0, uint8_t* dst_arr) {
-    const __amdgpu_buffer_rsrc_t rsrc = tile_rsrc(base, stride, kv0);
+  auto dma_k = [&](int kv0, int slot) {
 #pragma unroll
-    for (int j = 0; j < kLoadsPerWave; ++j) dma_one(rsrc, stride, offs, j, dst_arr);
+    for (int j = 0; j < kLoadsPerWave; ++j) dma_one(krsrc, kstride, koffs, kv0, j, kslot(slot));
   };
-  auto dma_k = [&](int kv0, int slot) { dma_rows(kbase, kstride, koffs, kv0, kslot(slot)); };
-  auto dma_v = [&](int kv0, int slot) { dma_rows(vbase, vstride, voffs, kv0, vslot(slot)); };
+  auto dma_v = [&](int kv0, int slot) {
+#pragma unroll
+    for (int j = 0; j < kLoadsPerWave; ++j) dma_one(vrsrc, vstride, voffs, kv0, j, vslot(slot));
+  };
   // first token of tile t, clamped to the task's tiles
   auto tile_kv0 = [&](int t) -> int { return kvt[t < 0 ? 0 : t < nkv_tiles ? t : nkv_tiles - 1] * TKV; };
 
@@ -351,6 +352,13 @@ void attn_fwd_kernel(AttnArgs a) {
   for (int g = 0; g < G; ++g) mem_row[g] = (a.gq > 1) ? (q_local(g) >> a.bq_shift) : 0;
   const int mem_bits = a.gq * a.gkv;
   const uint64_t full = (mem_bits >= 64) ? ~0ull : ((1ull << mem_bits) - 1);
+  // membership bits of tile t: the plan's bitmap, or, for plans that record
+  // none, the zero page inverted (every member active); no branch, so the
+  // scalar loads of one iteration issue together
+  const cu64p mbits = a.member ? (cu64p)(a.member + tb) : (cu64p)a.zero_page;
+  const int mstep = a.member ? 1 : 0;
+  const uint64_t minv = a.member ? 0ull : ~0ull;
+  auto bits_of = [&](int t) -> uint64_t { return (mbits[t * mstep] ^ minv) & full; };
   const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
   f32x16 o[G][4];
@@ -479,9 +487,7 @@ void attn_fwd_kernel(AttnArgs a) {
   auto iteration = [&](f32x16* s_cur, f32x16* s_nxt, int kv0_cur, uint64_t bits_cur, const uint8_t* ks_next,
                        const uint8_t* vs_prev, u32x4* pw_cur, const u32x4* pw_prev, int kv0_refill_k,
                        int kv0_refill_v, uint8_t* k_refill, uint8_t* v_refill, bool* active, float* lsum) {
-    // the ring refill of this iteration, one load every kDmaEvery units
-    const __amdgpu_buffer_rsrc_t rk = tile_rsrc(kbase, kstride, kv0_refill_k);
-    const __amdgpu_buffer_rsrc_t rv = tile_rsrc(vbase, vstride, kv0_refill_v);
+    // the ring refill of this iteration goes out one load every kDmaEvery units
 #pragma unroll
     for (int g = 0; g < G; ++g) active[g] = true;
     if (__builtin_expect(kv0_cur + TKV > a.Nkv || bits_cur != full, 0)) {
@@ -520,8 +526,8 @@ void attn_fwd_kernel(AttnArgs a) {
         if (u + kAhead < kNU) op[(u + kAhead) % (kAhead + 1)] = load_op(u + kAhead, ks_next, vs_prev);
         if (u % kDmaEvery == 0 && u / kDmaEvery < kGroupLoads) {
           const int i = u / kDmaEvery;
-          if (i < kLoadsPerWave) dma_one(rk, kstride, koffs, i, k_refill);
-          else dma_one(rv, vstride, voffs, i - kLoadsPerWave, v_refill);
+          if (i < kLoadsPerWave) dma_one(krsrc, kstride, koffs, kv0_refill_k, i, k_refill);
+          else dma_one(vrsrc, vstride, voffs, kv0_refill_v, i - kLoadsPerWave, v_refill);
         }
       }
       if (u < kNA) {
@@ -602,7 +608,7 @@ void attn_fwd_kernel(AttnArgs a) {
     kv_next_k = tile_kv0(STAGES);
     kv_next_v = tile_kv0(STAGES - 2);
     kv_cur = tile_kv0(0);
-    bits_cur = mbits ? mbits[0] : full;
+    bits_cur = bits_of(0);
     // the scores of tile 0 need K0 only
     wait_vm_lgkm<(STAGES - 1) * kGroup>();
     block_sync();
@@ -631,20 +637,19 @@ void attn_fwd_kernel(AttnArgs a) {
       float lsum[G];
       iteration(s_cur, s_nxt, kv_cur, bits_cur, kslot((u + 1) % STAGES), vslot((u + 1) % STAGES), pw_cur, pw_prev,
                 kv_next_k, kv_next_v, kslot(u), vslot(u), active, lsum);
-      // the check of tile t before any MFMA uses its probabilities (NaN-safe)
-      bool need[G], any = false;
+      // the check of tile t before any MFMA uses its probabilities (sums of
+      // probabilities in [0, inf] are never NaN)
+      auto needs_raise = [&](int g) { return lsum[g] > kSumMax || (m_run[g] == kNegInf && active[g]); };
+      uint64_t need_any = 0;
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
-        need[g] = !(lsum[g] <= kSumMax) || (m_run[g] == kNegInf && active[g]);
-        any = any || need[g];
-      }
-      if (__builtin_expect(__ballot(any) != 0, 0)) {
+      for (int g = 0; g < G; ++g) need_any |= __ballot(needs_raise(g));
+      if (__builtin_expect(need_any != 0, 0)) {
 #pragma unroll
         for (int g = 0; g < G; ++g) {
           // both lane halves of a row take the same decision; the exchange
-          // runs in every lane (a short-circuit || would run it only where
-          // need is false, and a lane swap there reads inactive partners)
-          const uint32_t mine = need[g] ? 1u : 0u;
+          // runs in every lane (under a short-circuit || it would run only in
+          // some lanes, and a lane swap there reads inactive partners)
+          const uint32_t mine = needs_raise(g) ? 1u : 0u;
           const bool row = (mine | other_half_u32(mine)) != 0;
           if (__ballot(row) != 0) lsum[g] = raise_reference(g, s_cur, pw_cur, row, lsum[g]);
         }
@@ -657,7 +662,7 @@ void attn_fwd_kernel(AttnArgs a) {
       kv_next_k = tile_kv0(t + 1 + STAGES);
       kv_next_v = tile_kv0(t + STAGES - 1);
       kv_cur = tile_kv0(t + 1);
-      bits_cur = mbits ? mbits[t + 1 < nkv_tiles ? t + 1 : nkv_tiles - 1] : full;
+      bits_cur = bits_of(t + 1 < nkv_tiles ? t + 1 : nkv_tiles - 1);
       asm volatile("" ::"s"(kv_next_k), "s"(kv_next_v), "s"(kv_cur), "s"(bits_cur));
       // slot (t+2) % STAGES must have landed; younger loads may fly
       wait_vm_lgkm<kInFlight>();

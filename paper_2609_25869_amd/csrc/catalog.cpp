@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <algorithm>
 
 namespace bsa {
 
@@ -56,6 +57,11 @@ const char* ineligible_reason(const CatalogEntry& e, int32_t bq, int32_t bkv, co
   for (const int64_t* st : strides)
     for (int i = 0; i < 3; ++i)
       if (st[i] < 0 || st[i] % 8 != 0) return "strides must be non-negative multiples of 8 elements (16 bytes)";
+  // the attention kernel addresses one head's K and V rows with 32-bit byte
+  // offsets (up to a tile past the sequence end)
+  const int64_t row_bytes = 2 * std::max(s.k_stride[2], s.v_stride[2]);
+  if (((int64_t)s.seq_kv + 64) * row_bytes + 256 > 0xFFFFFFFFll)
+    return "the K/V rows of one head must span less than 4 GiB";
   if (!nests(e.tq, bq)) return "query tile and query block do not nest";
   if (!nests(e.tkv, bkv)) return "KV tile and KV block do not nest";
   const int64_t gq = e.tq >= bq ? e.tq / bq : 1, gkv = e.tkv >= bkv ? e.tkv / bkv : 1;

@@ -151,6 +151,20 @@ def features_of(z):
             "density": (z.nnz, z.blocks), "run_coverage": (z.run_blocks, z.nnz)}
 
 
+def test_kv_rows_of_one_head_must_fit_32_bit_offsets():
+    """K and V rows of a head are addressed with 32-bit byte offsets, up to
+    a tile past the sequence end: larger requests have no eligible plan."""
+    # [B, N, H, 128] bf16: a token row of all heads is H * 256 bytes
+    ok = bsa.make_shapes(1, 24, 1024, 131072)              # 131136 * 6144 B = 0.75 GiB
+    assert all(bsa.plan_eligible(p, 64, 64, ok) for p in range(24))
+    big = bsa.make_shapes(1, 64, 1024, 300000)              # 300064 * 16384 B > 4 GiB
+    assert not any(bsa.plan_eligible(p, 64, 64, big) for p in range(24))
+    # the limit is on the token stride of K and V, not on the head count
+    edge_rows = (0xFFFFFFFF - 256) // (2 * 24 * 128) - 64
+    assert bsa.plan_eligible(4, 64, 64, bsa.make_shapes(1, 24, 64, edge_rows))
+    assert not bsa.plan_eligible(4, 64, 64, bsa.make_shapes(1, 24, 64, edge_rows + 1))
+
+
 def test_lut_rank_and_select_match_the_reference(tmp_path):
     table, base = synthetic_table()
     assert table
