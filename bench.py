@@ -132,6 +132,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--force-plan", type=int, default=-1)
     ap.add_argument("--no-flush", action="store_true", help="skip the cache-evicting write before each step")
+    ap.add_argument("--sparsify", action="store_true",
+                    help="top-k workloads: build the mask on the device inside every request "
+                         "(bsa_sparsify_topk -> bsa_plan -> bsa_forward) instead of reading a resident one")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (HBM counter calibration) and exit")
     args = ap.parse_args()
@@ -163,6 +166,18 @@ def main():
     lse = torch.empty((cfg.B, cfg.H, cfg.N), dtype=torch.float32, device=dev)
     md = torch.from_numpy(mask.data).to(dev)
     shapes = bsa.shapes_of(qd, kd, vd, od)
+    topk = None
+    if args.sparsify:
+        if cfg.kind != "topk":
+            print("--sparsify applies to the top-k workloads only", file=sys.stderr)
+            sys.exit(2)
+        bq0, bkv0 = cfg.geometry[0]
+        topk = int(np.floor(cfg.params["frac"] * (-(-cfg.N // bkv0)) + 0.5))
+        dev_mask = bsa.sparsify_topk(qd, kd, bq0, bkv0, topk)
+        torch.cuda.synchronize()
+        # the device sparsifier reproduces the workload's mask recipe; report any difference
+        n_diff = int((dev_mask.cpu().numpy().reshape(-1) != mask.data.reshape(-1)).sum())
+        log("device sparsifier: %d of %d mask entries differ from the workload mask" % (n_diff, mask.data.size))
     per_head = not mask.uniform_geometry
     bq = [int(x) for x in mask.bq] if per_head else int(mask.bq[0])
     bkv = [int(x) for x in mask.bkv] if per_head else int(mask.bkv[0])
@@ -172,9 +187,19 @@ def main():
     flush = None if args.no_flush else torch.empty(FLUSH_BYTES // 4, dtype=torch.int32, device=dev)
     torch.cuda.synchronize()
 
+    sp_ms = []
+
     def request():
         if flush is not None:
             flush.fill_(1)
+        if topk is not None:
+            s0 = torch.cuda.Event(enable_timing=True)
+            s1 = torch.cuda.Event(enable_timing=True)
+            s0.record(stream)
+            bsa.sparsify_topk(qd, kd, cfg.geometry[0][0], cfg.geometry[0][1], topk, mask=md.view(dev_mask.shape),
+                              stream=stream)
+            s1.record(stream)
+            sp_ms.append((s0, s1))
         p = bsa.plan(md, bq, bkv, shapes, head_offset=list(mask.head_offset), stride_b=mask.stride_b,
                      force_plan=args.force_plan, stream=stream)
         e0 = torch.cuda.Event(enable_timing=True)
@@ -262,6 +287,10 @@ def main():
             "kv_stream_gbs": tiles_bytes / (k_avg * 1e-3) / 1e9,
         },
     }
+    if topk is not None:
+        sp = [a.elapsed_time(b) for a, b in sp_ms[-args.steps:]]
+        out["sparsify_ms"] = {"mean": float(np.mean(sp)), "median": float(np.median(sp)), "topk": topk,
+                              "in_request": True}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle (about %.0f s)" % args.cpu_budget)
         out["cpu_baseline"] = cpu_baseline(q, k, v, mask, eff, args.cpu_budget)

@@ -225,6 +225,35 @@ BSA_API bsa_status bsa_plan_export(bsa_plan_t plan, int32_t segment, int32_t wha
 /* Release a plan (stream-ordered on the plan's stream). */
 BSA_API bsa_status bsa_plan_destroy(bsa_plan_t plan);
 
+/*
+ * Top-k block sparsifier: the step before bsa_plan that supplies the logical
+ * mask M for geometry (bq, bkv) (Section 2.1: the sparsifier hands M and B to
+ * the runtime), so that sparsify -> plan -> forward stays on the device.
+ * For every (b, h) and query block qb, KV block kb scores
+ *     s = sum_c mean(Q rows of qb)[c] * mean(K rows of kb)[c]
+ * (a ragged last block averages the rows it has); the `topk` largest scores
+ * of each row are active, ties going to the lower kb, and with diagonal != 0
+ * every block that the token diagonal i == j passes through is added.  The
+ * scores are computed in IEEE double, block sums in token order, the sum
+ * over c in increasing order with one rounding per multiply and per add, so
+ * the selection is reproducible bit for bit off the device.
+ *
+ * q: [batch, seq_q, heads, 128] and k: [batch, seq_kv, heads, 128] bf16,
+ * device, strides from `shapes` (v and o strides are ignored).  mask: device
+ * uint8 [batch, heads, ceil(seq_q / bq), ceil(seq_kv / bkv)], contiguous,
+ * caller-owned, written entirely (1 = active); for bsa_plan pass
+ * head_offset[h] = h * nqb * nkb and stride_b = heads * nqb * nkb.
+ * topk <= 0 selects no block by score, topk >= nkb every block.
+ * Errors: BSA_ERR_INVALID for null pointers, non-positive geometry or bad
+ * shapes; BSA_ERR_UNSUPPORTED for a dtype other than bf16, a head dim other
+ * than 128, or more than 6144 KV blocks per row.  Scratch memory (block
+ * means and score rows of up to 256 MiB of heads at a time) is taken from
+ * the device's stream-ordered pool and returned on `stream`.  Asynchronous
+ * on `stream`.
+ */
+BSA_API bsa_status bsa_sparsify_topk(const void* q, const void* k, const bsa_shapes* shapes, int32_t bq,
+                                     int32_t bkv, int32_t topk, int32_t diagonal, uint8_t* mask, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -82,3 +82,24 @@ def select(table: Dict[Key, Dict[Bucket, List[int]]], key: Key, bucket: Bucket,
         if eligible(p):
             return p
     return None
+
+
+def region_contains(features: Dict[str, object], region: Sequence[Tuple[Optional[int], Optional[int]]],
+                    names: Sequence[str]) -> bool:
+    """Regimes given as leaves of a decision tree (Section 5.1): one
+    half-open interval [lo, hi) per feature, None for an unbounded side.
+    Ratio features compare exactly as integers, num * 10000 >= edge * den."""
+    for name, (lo, hi) in zip(names, region):
+        v = features[name]
+        if isinstance(v, tuple):
+            num, den = v
+            if den == 0:
+                num, den = 0, 1
+            at_least = lambda e: num * 10000 >= e * den
+        else:
+            at_least = lambda e: v >= e
+        if lo is not None and not at_least(lo):
+            return False
+        if hi is not None and at_least(hi):
+            return False
+    return True

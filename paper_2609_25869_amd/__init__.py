@@ -247,3 +247,30 @@ def forward(p: Plan, q, k, v, o, lse=None, stream=None):
                             ctypes.c_void_p(lse.data_ptr()) if lse is not None else None,
                             _stream_handle(stream)))
     return o
+
+
+def sparsify_topk(q, k, bq: int, bkv: int, topk: int, diagonal: bool = True, mask=None, stream=None):
+    """Mean-pooled top-k block mask of bf16 [B, N, H, 128] tensors q and k
+    (bsa_sparsify_topk): uint8 [B, H, ceil(Nq / bq), ceil(Nkv / bkv)] on the
+    device, written into `mask` when given.  Pass it to plan() with
+    head_offset = [h * nqb * nkb] and stride_b = H * nqb * nkb."""
+    import torch
+    for t in (q, k):
+        if not t.is_cuda or t.dtype != torch.bfloat16 or t.dim() != 4 or t.stride(3) != 1:
+            raise TypeError("q and k must be CUDA bfloat16 [B, N, H, d] tensors with d contiguous")
+    B, Nq, H, d = q.shape
+    Nkv = k.shape[1]
+    if tuple(k.shape) != (B, Nkv, H, d):
+        raise ValueError("inconsistent q/k shapes")
+    nqb, nkb = -(-Nq // int(bq)), -(-Nkv // int(bkv))
+    if mask is None:
+        mask = torch.empty((B, H, nqb, nkb), dtype=torch.uint8, device=q.device)
+    elif (tuple(mask.shape) != (B, H, nqb, nkb) or mask.dtype != torch.uint8 or not mask.is_cuda
+          or not mask.is_contiguous()):
+        raise ValueError("mask must be a contiguous CUDA uint8 tensor of shape %s" % ((B, H, nqb, nkb),))
+    st = lambda t: (t.stride(0), t.stride(2), t.stride(1))
+    shapes = make_shapes(B, H, Nq, Nkv, d, st(q), st(k), st(k), st(q))
+    _check(_lib.bsa_sparsify_topk(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()), ctypes.byref(shapes),
+                                  int(bq), int(bkv), int(topk), 1 if diagonal else 0, ctypes.c_void_p(mask.data_ptr()),
+                                  _stream_handle(stream)))
+    return mask

@@ -115,5 +115,17 @@ hipError_t launch_attention(int tq, int tkv, const AttnArgs& a, hipStream_t s);
 bool attention_variant_exists(int tq, int tkv);
 hipError_t launch_splitk_merge(int tq, const AttnArgs& a, hipStream_t s);
 
+// Top-k sparsifier (sparsify.hip): block means of a [B, N, H, 128] bf16
+// tensor for heads [bh0, bh0 + nbh) into out[nbh][ceil(N / blk)][128] (fp64),
+// the score rows of those heads, and the uint8 mask rows they select.
+int32_t sparsify_max_kv_blocks();
+hipError_t launch_block_mean(const uint16_t* x, int64_t s0, int64_t s1, int64_t s2, int32_t H, int32_t n,
+                             int32_t blk, int32_t bh0, int32_t nbh, double* out, hipStream_t s);
+hipError_t launch_block_scores(const double* pq, const double* pk, int32_t nqb, int32_t nkb, int32_t nbh,
+                               double* scores, hipStream_t s);
+hipError_t launch_topk_select(const double* scores, int32_t nqb, int32_t nkb, int32_t k, int32_t diagonal,
+                              int32_t nq, int32_t nkv, int32_t bq, int32_t bkv, int32_t bh0, int32_t nbh,
+                              uint8_t* mask, hipStream_t s);
+
 
 }  // namespace bsa

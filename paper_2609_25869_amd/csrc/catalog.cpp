@@ -221,6 +221,64 @@ bool known_feature(const std::string& n) {
   return false;
 }
 
+bool read_ranking(const JVal* v, std::vector<int32_t>* rk, std::string* err) {
+  std::vector<int64_t> ids;
+  if (!as_int_list(v, &ids) || ids.empty()) { *err = "bad ranking"; return false; }
+  rk->clear();
+  for (int64_t id : ids) {
+    if (!catalog_find((int32_t)id)) { *err = "ranking names an unknown plan"; return false; }
+    rk->push_back((int32_t)id);
+  }
+  return true;
+}
+
+// Version 2: "features" lists the feature names; each regime has a "region",
+// one [lo, hi] pair per feature with null for an unbounded side.
+bool parse_regions(const JVal& root, Lut* out, std::string* err) {
+  const JVal* feats = root.get("features");
+  if (!feats || feats->kind != JVal::kArr || feats->arr.empty()) { *err = "missing feature list"; return false; }
+  out->feature_names.clear();
+  out->feature_edges.clear();
+  for (const auto& f : feats->arr) {
+    if (f.kind != JVal::kStr || !known_feature(f.str)) { *err = "unknown feature"; return false; }
+    out->feature_names.push_back(f.str);
+  }
+  const size_t nf = out->feature_names.size();
+  const JVal* regimes = root.get("regimes");
+  if (!regimes || regimes->kind != JVal::kArr) { *err = "missing regimes"; return false; }
+  out->regions.clear();
+  for (const auto& r : regimes->arr) {
+    std::vector<int64_t> key;
+    const JVal* reg = r.kind == JVal::kObj ? r.get("region") : nullptr;
+    if (r.kind != JVal::kObj || !as_int_list(r.get("key"), &key) || key.size() != 4 || !reg ||
+        reg->kind != JVal::kArr || reg->arr.size() != nf) {
+      *err = "bad regime entry";
+      return false;
+    }
+    Lut::Region g;
+    for (const auto& iv : reg->arr) {
+      if (iv.kind != JVal::kArr || iv.arr.size() != 2) { *err = "bad region interval"; return false; }
+      int64_t b[2] = {0, 0};
+      char has[2] = {0, 0};
+      for (int j = 0; j < 2; ++j) {
+        const JVal& x = iv.arr[j];
+        if (x.kind == JVal::kNull) continue;
+        if (x.kind != JVal::kNum || x.num != std::floor(x.num)) { *err = "bad region bound"; return false; }
+        b[j] = (int64_t)x.num;
+        has[j] = 1;
+      }
+      if (has[0] && has[1] && b[1] <= b[0]) { *err = "empty region interval"; return false; }
+      g.lo.push_back(b[0]);
+      g.hi.push_back(b[1]);
+      g.has_lo.push_back(has[0]);
+      g.has_hi.push_back(has[1]);
+    }
+    if (!read_ranking(r.get("ranking"), &g.ranking, err)) return false;
+    out->regions[key].push_back(std::move(g));
+  }
+  return true;
+}
+
 }  // namespace
 
 bool lut_parse(const std::string& text, Lut* out, std::string* err) {
@@ -233,8 +291,11 @@ bool lut_parse(const std::string& text, Lut* out, std::string* err) {
   const JVal* fmt = root.get("format");
   if (!fmt || fmt->kind != JVal::kStr || fmt->str != "bsa-plan-table") { *err = "not a bsa-plan-table artifact"; return false; }
   const JVal* ver = root.get("version");
-  if (!ver || ver->kind != JVal::kNum || (int)ver->num != 1) { *err = "unsupported artifact version"; return false; }
-  out->version = 1;
+  if (!ver || ver->kind != JVal::kNum || ((int)ver->num != 1 && (int)ver->num != 2)) {
+    *err = "unsupported artifact version";
+    return false;
+  }
+  out->version = (int)ver->num;
   const JVal* arch = root.get("arch");
   if (!arch || arch->kind != JVal::kStr || arch->str != "gfx950") { *err = "artifact is not for gfx950"; return false; }
   out->arch = arch->str;
@@ -253,6 +314,7 @@ bool lut_parse(const std::string& text, Lut* out, std::string* err) {
       return false;
     }
   }
+  if (out->version == 2) return parse_regions(root, out, err);
   const JVal* schema = root.get("schema");
   if (!schema || schema->kind != JVal::kArr) { *err = "missing feature schema"; return false; }
   out->feature_names.clear();
@@ -310,9 +372,42 @@ std::vector<int64_t> lut_bucket(const Lut& lut, const bsa_regime_query& z) {
   return b;
 }
 
+namespace {
+
+// feature `n` of z >= edge (ratio features exactly, edges in units of 1e-4)
+bool feature_ge(const std::string& n, const bsa_regime_query& z, int64_t edge) {
+  if (n == "density" || n == "run_coverage") {
+    int64_t num = n == "density" ? z.nnz : z.run_blocks;
+    int64_t den = n == "density" ? z.blocks : z.nnz;
+    if (den <= 0) { num = 0; den = 1; }
+    return (__int128)num * 10000 >= (__int128)edge * den;
+  }
+  const int64_t v = n == "seq_q" ? z.seq_q : n == "seq_kv" ? z.seq_kv : z.batch_heads;
+  return v >= edge;
+}
+
+}  // namespace
+
 std::vector<int32_t> lut_ranking(const Lut* lut, const bsa_regime_query& z, bool* hit) {
   *hit = false;
-  if (lut) {
+  if (lut && lut->version == 2) {
+    const std::vector<int64_t> key{z.bq, z.bkv, z.dtype, z.head_dim};
+    auto it = lut->regions.find(key);
+    if (it != lut->regions.end()) {
+      for (const Lut::Region& g : it->second) {
+        bool in = true;
+        for (size_t f = 0; f < lut->feature_names.size() && in; ++f) {
+          const std::string& n = lut->feature_names[f];
+          if (g.has_lo[f] && !feature_ge(n, z, g.lo[f])) in = false;
+          if (in && g.has_hi[f] && feature_ge(n, z, g.hi[f])) in = false;
+        }
+        if (in) {
+          *hit = true;
+          return g.ranking;
+        }
+      }
+    }
+  } else if (lut) {
     const std::vector<int64_t> key{z.bq, z.bkv, z.dtype, z.head_dim};
     auto it = lut->table.find(key);
     if (it != lut->table.end()) {

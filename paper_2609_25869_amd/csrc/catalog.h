@@ -37,8 +37,17 @@ struct Lut {
   // feature schema: names and bucket edges (ratio features in units of 1e-4)
   std::vector<std::string> feature_names;
   std::vector<std::vector<int64_t>> feature_edges;
-  // (bq, bkv, dtype, head_dim) -> bucket tuple -> ranking
+  // version 1: (bq, bkv, dtype, head_dim) -> bucket tuple -> ranking
   std::map<std::vector<int64_t>, std::map<std::vector<int64_t>, std::vector<int32_t>>> table;
+  // version 2: the regimes of a key are disjoint regions, one half-open
+  // interval [lo, hi) per feature (has_lo / has_hi false = unbounded), the
+  // leaves of a decision tree learned offline
+  struct Region {
+    std::vector<int64_t> lo, hi;
+    std::vector<char> has_lo, has_hi;
+    std::vector<int32_t> ranking;
+  };
+  std::map<std::vector<int64_t>, std::vector<Region>> regions;
 };
 
 // Parse an artifact; on failure returns false and fills *err.

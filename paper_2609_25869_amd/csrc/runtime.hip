@@ -14,6 +14,7 @@
 #include <memory>
 #include <mutex>
 #include <sstream>
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -889,6 +890,55 @@ bsa_status bsa_plan_export(bsa_plan_t plan, int32_t segment, int32_t what, void*
 
 bsa_status bsa_plan_destroy(bsa_plan_t plan) {
   delete plan;
+  return BSA_OK;
+}
+
+bsa_status bsa_sparsify_topk(const void* q, const void* k, const bsa_shapes* shapes, int32_t bq, int32_t bkv,
+                             int32_t topk, int32_t diagonal, uint8_t* mask, void* stream_in) {
+  if (!q || !k || !mask) return fail(BSA_ERR_INVALID, "q, k and mask must be device pointers");
+  bsa_status st = validate_shapes(shapes);
+  if (st != BSA_OK) return st;
+  if (bq < 1 || bkv < 1) return fail(BSA_ERR_INVALID, "block sizes must be positive");
+  const bsa_shapes& s = *shapes;
+  if (s.dtype != BSA_DTYPE_BF16) return fail(BSA_ERR_UNSUPPORTED, "only bfloat16 tensors are implemented");
+  if (s.head_dim != kHeadDim) return fail(BSA_ERR_UNSUPPORTED, "only head_dim 128 is implemented");
+  const int64_t nqb = cdiv(s.seq_q, bq), nkb = cdiv(s.seq_kv, bkv);
+  if (nkb > sparsify_max_kv_blocks())
+    return fail(BSA_ERR_UNSUPPORTED, "more than " + std::to_string(sparsify_max_kv_blocks()) + " KV blocks per row");
+  hipStream_t stream = (hipStream_t)stream_in;
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  prepare_pool(dev);
+  const int64_t nbh = (int64_t)s.batch * s.heads;
+  // heads per pass: score rows of at most 256 MiB
+  const int64_t per_head = nqb * nkb * (int64_t)sizeof(double);
+  const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(nbh, (int64_t(256) << 20) / per_head));
+  const size_t bytes_q = (size_t)(chunk * nqb * kHeadDim) * sizeof(double);
+  const size_t bytes_k = (size_t)(chunk * nkb * kHeadDim) * sizeof(double);
+  const size_t bytes_s = (size_t)(chunk * per_head);
+  void* scratch = nullptr;
+  HIP_TRY(hipMallocAsync(&scratch, bytes_q + bytes_k + bytes_s, stream));
+  double* pq = static_cast<double*>(scratch);
+  double* pk = reinterpret_cast<double*>(static_cast<uint8_t*>(scratch) + bytes_q);
+  double* sc = reinterpret_cast<double*>(static_cast<uint8_t*>(scratch) + bytes_q + bytes_k);
+  const uint16_t* qh = static_cast<const uint16_t*>(q);
+  const uint16_t* kh = static_cast<const uint16_t*>(k);
+  hipError_t e = hipSuccess;
+  for (int64_t bh0 = 0; bh0 < nbh && e == hipSuccess; bh0 += chunk) {
+    const int32_t n = (int32_t)std::min<int64_t>(chunk, nbh - bh0);
+    e = launch_block_mean(qh, s.q_stride[0], s.q_stride[1], s.q_stride[2], s.heads, s.seq_q, bq, (int32_t)bh0, n, pq,
+                          stream);
+    if (e == hipSuccess)
+      e = launch_block_mean(kh, s.k_stride[0], s.k_stride[1], s.k_stride[2], s.heads, s.seq_kv, bkv, (int32_t)bh0, n,
+                            pk, stream);
+    if (e == hipSuccess) e = launch_block_scores(pq, pk, (int32_t)nqb, (int32_t)nkb, n, sc, stream);
+    if (e == hipSuccess)
+      e = launch_topk_select(sc, (int32_t)nqb, (int32_t)nkb, topk, diagonal ? 1 : 0, s.seq_q, s.seq_kv, bq, bkv,
+                             (int32_t)bh0, n, mask, stream);
+  }
+  const hipError_t ef = hipFreeAsync(scratch, stream);
+  if (e != hipSuccess) return fail(BSA_ERR_HIP, std::string("sparsifier launch: ") + hipGetErrorString(e));
+  if (ef != hipSuccess) return fail(BSA_ERR_HIP, std::string("hipFreeAsync: ") + hipGetErrorString(ef));
   return BSA_OK;
 }
 

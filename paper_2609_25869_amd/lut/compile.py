@@ -139,16 +139,93 @@ def regret_report(table, schema, base_plan, records) -> Dict:
             "per_key": {k: summary(v) for k, v in sorted(per_key.items())}}
 
 
+def artifact_v2(regions, catalog, provenance: Dict) -> Dict:
+    """Version-2 artifact: per key, the decision-tree leaves as disjoint regions."""
+    from . import tree
+    regimes = []
+    for key in sorted(regions):
+        for region, ranking, n in regions[key]["regimes"]:
+            regimes.append({"key": list(key), "region": [[lo, hi] for lo, hi in region], "ranking": ranking,
+                            "cases": n})
+    return {
+        "format": "bsa-plan-table",
+        "version": 2,
+        "arch": "gfx950",
+        "catalog": [[e["id"], e["tq"], e["tkv"], e["split"], e["stages"], e["waves"]] for e in catalog],
+        "features": list(tree.FEATURES),
+        "regimes": regimes,
+        "depths": {"%d:%d" % key[:2]: regions[key]["depth"] for key in sorted(regions)},
+        "provenance": provenance,
+    }
+
+
+def regret_report_v2(regions, base_plan, records) -> Dict:
+    """Selected / fastest measured latency per case for a region table."""
+    from . import tree
+    regrets, misses, per_key = [], 0, {}
+    for r in records:
+        lat = {int(p): t for p, t in r["latency_ms"].items()}
+        if not lat:
+            continue
+        base = base_plan(tuple(r["key"]))
+        rk, hit = tree.select(regions, r["key"], r["features"], base)
+        misses += not hit
+        sel = next((p for p in rk if p in lat), None)
+        g = lat[sel] / min(lat.values()) if sel is not None else float("nan")
+        regrets.append(g)
+        per_key.setdefault("%d:%d" % tuple(r["key"][:2]), []).append(g)
+    return _regret_summary(regrets, misses, per_key)
+
+
+def _regret_summary(regrets, misses, per_key):
+    regrets = [g for g in regrets if g == g]
+
+    def summary(xs):
+        xs = sorted(g for g in xs if g == g)
+        if not xs:
+            return {}
+        pct = lambda q: xs[min(len(xs) - 1, int(math.ceil(q * len(xs))) - 1)]
+        return {"cases": len(xs), "gm": math.exp(sum(math.log(x) for x in xs) / len(xs)), "p95": pct(0.95),
+                "p99": pct(0.99), "max": xs[-1], "within_3pct": sum(1 for x in xs if x <= 1.03) / len(xs)}
+
+    return {"all": summary(regrets), "lookup_misses": misses,
+            "per_key": {k: summary(v) for k, v in sorted(per_key.items())}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--profile", default=os.path.join(HERE, "gfx950_profile.jsonl"))
     ap.add_argument("--eval", default=os.path.join(HERE, "gfx950_eval.jsonl"))
-    ap.add_argument("--out", default=os.path.join(HERE, "gfx950_v1.json"))
+    ap.add_argument("--out", default=None)
+    ap.add_argument("--tree", action="store_true",
+                    help="learn the regimes with per-key decision trees (version-2 artifact)")
     args = ap.parse_args()
     import paper_2609_25869_amd as bsa
 
     base = lambda key: bsa.base_plan(key[0], key[1])
     recs = load_records(args.profile)
+    if args.tree:
+        from . import tree
+        regions = tree.compile_regions(recs, base)
+        prov = {"profiled_on": "MI355X (gfx950)", "profile_cases": len(recs),
+                "regimes": "per-key regret decision trees, >= %d cases per leaf, depth by source-grouped 4-fold "
+                           "cross-validation over %s" % (tree.MIN_LEAF, list(tree.DEPTHS)),
+                "latency": "median of 3 kernel runs after 1 warm-up, HIP events"}
+        if os.path.exists(args.eval):
+            ev = load_records(args.eval)
+            prov["eval_cases"] = len(ev)
+            prov["eval_regret"] = regret_report_v2(regions, base, ev)["all"]
+        prov["profile_regret"] = regret_report_v2(regions, base, recs)["all"]
+        doc = artifact_v2(regions, bsa.catalog(), prov)
+        with open(args.out or os.path.join(HERE, "gfx950_v2.json"), "w") as f:
+            json.dump(doc, f, indent=1)
+            f.write("\n")
+        print(json.dumps(prov, indent=1))
+        print(json.dumps(doc["depths"]))
+        if os.path.exists(args.eval):
+            print(json.dumps(regret_report_v2(regions, base, load_records(args.eval)), indent=1))
+        return
+    args.out = args.out or os.path.join(HERE, "gfx950_v1.json")
     table = compile_table(recs, SCHEMA, base)
     prov = {"profiled_on": "MI355X (gfx950)", "profile_cases": len(recs),
             "corpus": "seeded synthetic masks (frame windows, Bernoulli + diagonal, pooled q.k top-k), "

@@ -33,9 +33,9 @@ def header_functions():
 def test_header_declares_the_request_entry_points():
     names = header_functions()
     for required in ("bsa_plan", "bsa_forward", "bsa_plan_destroy", "bsa_lut_load", "bsa_plan_export",
-                     "bsa_plan_info", "bsa_status_string", "bsa_last_error"):
+                     "bsa_plan_info", "bsa_status_string", "bsa_last_error", "bsa_sparsify_topk"):
         assert required in names
-    assert len(names) == 18
+    assert len(names) == 19
 
 
 def test_library_exports_exactly_the_header():
@@ -149,6 +149,22 @@ def synthetic_table(seed=0):
 def features_of(z):
     return {"seq_q": z.seq_q, "seq_kv": z.seq_kv, "batch_heads": z.batch_heads,
             "density": (z.nnz, z.blocks), "run_coverage": (z.run_blocks, z.nnz)}
+
+
+def test_sparsifier_rejects_bad_requests_before_any_launch():
+    """Argument errors surface before any device work (null pointers, block
+    sizes, dtype, head dim, KV blocks per row)."""
+    s = bsa.make_shapes(1, 2, 1024, 1024)
+    fake = ctypes.c_void_p(16)      # never dereferenced: every case fails validation first
+    call = lambda q, k, sh, bq, bkv, m: bsa._lib.bsa_sparsify_topk(q, k, ctypes.byref(sh), bq, bkv, 4, 1, m, None)
+    assert call(None, fake, s, 64, 64, fake) == _ffi.BSA_ERR_INVALID
+    assert call(fake, fake, s, 64, 64, None) == _ffi.BSA_ERR_INVALID
+    assert call(fake, fake, s, 0, 64, fake) == _ffi.BSA_ERR_INVALID
+    assert call(fake, fake, bsa.make_shapes(1, 2, 1024, 1024, head_dim=64), 64, 64, fake) == _ffi.BSA_ERR_UNSUPPORTED
+    assert call(fake, fake, bsa.make_shapes(1, 2, 1024, 1024, dtype=_ffi.DTYPE_F16), 64, 64, fake) == \
+        _ffi.BSA_ERR_UNSUPPORTED
+    assert call(fake, fake, bsa.make_shapes(1, 2, 64, 6145 * 16), 16, 16, fake) == _ffi.BSA_ERR_UNSUPPORTED
+    assert b"KV blocks per row" in bsa._lib.bsa_last_error()
 
 
 def test_kv_rows_of_one_head_must_fit_32_bit_offsets():
