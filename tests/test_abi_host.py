@@ -218,7 +218,7 @@ def test_density_bucket_edges_are_exact_integers(tmp_path):
 
 @pytest.mark.parametrize("mutate,needle", [
     (lambda d: d.update(format="other"), "artifact"),
-    (lambda d: d.update(version=2), "version"),
+    (lambda d: d.update(version=3), "version"),
     (lambda d: d.update(arch="gfx942"), "gfx950"),
     (lambda d: d["catalog"].pop(), "catalog"),
     (lambda d: d["catalog"][3].__setitem__(2, 999), "catalog"),
