@@ -1,0 +1,205 @@
+"""Plan-selection ablation on complete requests (Section 6, A0 / A1 / A2).
+
+  A0  Direct: the key's base plan (physical tile = logical block when the
+      catalog has it), prepared on every pass.
+  A1  Exhaustive online search: on the first (cold) pass every eligible
+      catalog plan is prepared and probed once, then the fastest is prepared
+      and executed; later (warm) passes prepare the cached winner again and
+      execute it.
+  A2  This runtime: bsa_plan selects one plan from the plan table and
+      prepares it; warm passes reuse the prepared plan.
+
+A pass is a complete request on resident inputs: wall time from the start of
+preparation to the end of execution (stream synchronised), mask and inputs
+already on the device.  Pass 1 is the cold unique request, passes 2-4 the
+warm exact repeats, and the amortized latency averages all four.  The
+kernel columns are the execution time of the plan each variant ends with.
+
+    python -m paper_2609_25869_amd.lut.ablation --out OUT.jsonl [--split eval] [--every 3] [--budget S]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import time
+
+from . import profile as prof
+
+PASSES = 4
+
+
+def _time_request(torch, stream, fn):
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    out = fn()
+    stream.synchronize()
+    return (time.perf_counter() - t0) * 1e3, out
+
+
+def _kernel_ms(torch, stream, bsa, p, q, k, v, o, reps=3):
+    ts = []
+    for _ in range(reps + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        bsa.forward(p, q, k, v, o, None, stream=stream)
+        e1.record(stream)
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return sorted(ts[1:])[len(ts[1:]) // 2]
+
+
+def run_case(torch, bsa, case):
+    bq, bkv = case["geometry"]
+    N, bh = case["N"], case["bh"]
+    dev = torch.device("cuda")
+    g = torch.Generator(device=dev)
+    g.manual_seed(case["seed"] + 7)
+    q = torch.randn((1, N, bh, 128), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    k = torch.randn((1, N, bh, 128), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    v = torch.randn((1, N, bh, 128), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    mask = prof.make_mask(torch, case, q, k)
+    nqb, nkb = mask.shape[1], mask.shape[2]
+    head_offset = [h * nqb * nkb for h in range(bh)]
+    shapes = bsa.shapes_of(q, k, v, q)
+    o = torch.empty_like(q)
+    stream = torch.cuda.current_stream()
+    base = bsa.base_plan(bq, bkv)
+    eligible = [e["id"] for e in bsa.catalog() if bsa.plan_eligible(e["id"], bq, bkv, shapes)]
+
+    def prepare(force):
+        return bsa.plan(mask, bq, bkv, shapes, head_offset=head_offset, stride_b=0, force_plan=force, stream=stream)
+
+    def execute(p):
+        bsa.forward(p, q, k, v, o, None, stream=stream)
+
+    def prepare_execute(force):
+        p = prepare(force)
+        execute(p)
+        return p
+
+    rec = {"id": case["id"], "key": [bq, bkv], "family": case["family"], "rho": case["rho"], "N": N, "bh": bh}
+
+    # A0: Direct, prepared on every pass
+    a0 = []
+    for _ in range(PASSES):
+        ms, p = _time_request(torch, stream, lambda: prepare_execute(base))
+        p.destroy()
+        a0.append(ms)
+
+    # A1: exhaustive online search, then the cached winner prepared again on warm passes
+    def search():
+        best, best_ms = None, math.inf
+        for pid in eligible:
+            try:
+                p = prepare(pid)
+            except bsa.BsaError:
+                continue
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            execute(p)
+            e1.record(stream)
+            e1.synchronize()
+            t = e0.elapsed_time(e1)
+            p.destroy()
+            if t < best_ms:
+                best, best_ms = pid, t
+        p = prepare(best)
+        execute(p)
+        return best, p
+
+    a1 = []
+    ms, (winner, p) = _time_request(torch, stream, search)
+    p.destroy()
+    a1.append(ms)
+    for _ in range(PASSES - 1):
+        ms, p = _time_request(torch, stream, lambda: prepare_execute(winner))
+        p.destroy()
+        a1.append(ms)
+
+    # A2: plan-table selection, the prepared plan reused on warm passes
+    ms, p2 = _time_request(torch, stream, lambda: prepare_execute(-1))
+    a2 = [ms]
+    for _ in range(PASSES - 1):
+        ms, _ = _time_request(torch, stream, lambda: execute(p2))
+        a2.append(ms)
+    chosen = p2.info(0)["plan_id"]
+
+    pa0, pa1 = prepare(base), prepare(winner)
+    rec.update({
+        "plans": {"A0": base, "A1": winner, "A2": chosen},
+        "request_ms": {"A0": a0, "A1": a1, "A2": a2},
+        "kernel_ms": {"A0": _kernel_ms(torch, stream, bsa, pa0, q, k, v, o),
+                      "A1": _kernel_ms(torch, stream, bsa, pa1, q, k, v, o),
+                      "A2": _kernel_ms(torch, stream, bsa, p2, q, k, v, o)},
+        "eligible": len(eligible),
+    })
+    for p in (pa0, pa1, p2):
+        p.destroy()
+    del q, k, v, o, mask
+    return rec
+
+
+def summarize(records):
+    """Paired-case geometric means of the latency ratios (Table 8 layout)."""
+    def gm(xs):
+        xs = [x for x in xs if x > 0 and x == x]
+        return math.exp(sum(math.log(x) for x in xs) / len(xs)) if xs else float("nan")
+
+    def pops(r, v):
+        ms = r["request_ms"][v]
+        return {"cold": ms[0], "warm": sum(ms[1:]) / (len(ms) - 1), "amortized": sum(ms) / len(ms)}
+
+    out = {"cases": len(records)}
+    for pop in ("cold", "warm", "amortized"):
+        out[pop] = {
+            "A0/A1": gm([pops(r, "A0")[pop] / pops(r, "A1")[pop] for r in records]),
+            "A1/A2": gm([pops(r, "A1")[pop] / pops(r, "A2")[pop] for r in records]),
+            "A0/A2": gm([pops(r, "A0")[pop] / pops(r, "A2")[pop] for r in records]),
+        }
+    out["kernel"] = {"A0/A1": gm([r["kernel_ms"]["A0"] / r["kernel_ms"]["A1"] for r in records]),
+                     "A0/A2": gm([r["kernel_ms"]["A0"] / r["kernel_ms"]["A2"] for r in records]),
+                     "A2/A1": gm([r["kernel_ms"]["A2"] / r["kernel_ms"]["A1"] for r in records])}
+    out["same_plan_as_A1"] = sum(r["plans"]["A1"] == r["plans"]["A2"] for r in records) / max(1, len(records))
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--out", required=True)
+    ap.add_argument("--split", default="eval", choices=sorted(prof.SPLIT_SEED))
+    ap.add_argument("--every", type=int, default=3, help="run every n-th case of the split")
+    ap.add_argument("--budget", type=float, default=600.0)
+    args = ap.parse_args()
+    import torch
+    import paper_2609_25869_amd as bsa
+
+    cases = prof.corpus(args.split)[::args.every]
+    done = set()
+    if os.path.exists(args.out):
+        done = {json.loads(l)["id"] for l in open(args.out) if l.strip()}
+    cases = [c for c in cases if c["id"] not in done]
+    prof.log("%d ablation cases" % len(cases))
+    # one request of every plan kind first, so no pass pays one-time setup
+    if cases:
+        run_case(torch, bsa, dict(cases[0], N=4096, bh=2))
+    t0 = time.time()
+    with open(args.out, "a") as f:
+        for c in cases:
+            if time.time() - t0 > args.budget:
+                prof.log("budget reached")
+                break
+            rec = run_case(torch, bsa, c)
+            f.write(json.dumps(rec) + "\n")
+            f.flush()
+            prof.log("%s %s N %d bh %d %s %.2f: cold A0 %.2f A1 %.2f A2 %.2f ms, plans %s" % (
+                c["id"], c["geometry"], c["N"], c["bh"], c["family"], c["rho"], rec["request_ms"]["A0"][0],
+                rec["request_ms"]["A1"][0], rec["request_ms"]["A2"][0], rec["plans"]))
+            torch.cuda.empty_cache()
+    recs = [json.loads(l) for l in open(args.out) if l.strip()]
+    print(json.dumps(summarize(recs), indent=1), flush=True)
+
+
+if __name__ == "__main__":
+    main()

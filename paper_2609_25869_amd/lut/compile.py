@@ -154,7 +154,8 @@ def artifact_v2(regions, catalog, provenance: Dict) -> Dict:
         "catalog": [[e["id"], e["tq"], e["tkv"], e["split"], e["stages"], e["waves"]] for e in catalog],
         "features": list(tree.FEATURES),
         "regimes": regimes,
-        "depths": {"%d:%d" % key[:2]: regions[key]["depth"] for key in sorted(regions)},
+        "partition": {"%d:%d" % key[:2]: {"kind": regions[key]["kind"], "depth": regions[key]["depth"],
+                                          "cv_regret": regions[key]["cv_regret"]} for key in sorted(regions)},
         "provenance": provenance,
     }
 
@@ -192,6 +193,47 @@ def _regret_summary(regrets, misses, per_key):
             "per_key": {k: summary(v) for k, v in sorted(per_key.items())}}
 
 
+def kernel_ablations(pick, base_plan, catalog, records) -> Dict:
+    """Kernel-time ablations from profiling records (Section 6).
+
+    A0 / A1 / A2: the key's base (Direct) plan, the fastest measured eligible
+    plan (what an exhaustive search finds), and the table's pick
+    (`pick(record)` -> ranking).  O0 / O1 / O2 hold the physical tile at the
+    base plan's tile and vary only the task organization (Split-K factor):
+    the base organization, the table's first-ranked plan with that tile, and
+    the fastest measured one.  Paired-case geometric means; wins / ties /
+    losses against O0 use a 3% tie band.
+    """
+    tile = {e["id"]: (e["tq"], e["tkv"]) for e in catalog}
+    gm = lambda xs: math.exp(sum(math.log(x) for x in xs) / len(xs)) if xs else float("nan")
+    a0a2, a0a1, a2a1, o_sp, o_reg, o1_reg, wtl = [], [], [], [], [], [], [0, 0, 0]
+    for r in records:
+        lat = {int(p): t for p, t in r["latency_ms"].items()}
+        base = base_plan(tuple(r["key"]))
+        if not lat or base not in lat:
+            continue
+        rk = pick(r)
+        sel = next((p for p in rk if p in lat), base)
+        best = min(lat.values())
+        a0a1.append(lat[base] / best)
+        a0a2.append(lat[base] / lat[sel])
+        a2a1.append(lat[sel] / best)
+        same = {p: t for p, t in lat.items() if tile[p] == tile[base]}
+        o1 = next((p for p in rk if p in same), base)
+        o2 = min(same.values())
+        o_sp.append(lat[base] / lat[o1])
+        o_reg.append(lat[base] / o2)
+        o1_reg.append(lat[o1] / o2)
+        ratio = lat[base] / lat[o1]
+        wtl[0 if ratio > 1.03 else 2 if ratio < 1 / 1.03 else 1] += 1
+    return {"cases": len(a0a1),
+            "kernel_speedup_over_A0": {"A1_exhaustive": gm(a0a1), "A2_table": gm(a0a2)},
+            "A2_regret_vs_A1": gm(a2a1),
+            "organization_at_base_tile": {"O1_speedup_over_O0": gm(o_sp), "O2_speedup_over_O0": gm(o_reg),
+                                          "O1_regret_vs_O2": gm(o1_reg), "O0_regret_vs_O2": gm(o_reg),
+                                          "O1_vs_O0_wins_ties_losses": wtl}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--profile", default=os.path.join(HERE, "gfx950_profile.jsonl"))
@@ -206,10 +248,11 @@ def main():
     recs = load_records(args.profile)
     if args.tree:
         from . import tree
-        regions = tree.compile_regions(recs, base)
+        regions = tree.compile_regions(recs, base, grid_schema=SCHEMA)
         prov = {"profiled_on": "MI355X (gfx950)", "profile_cases": len(recs),
-                "regimes": "per-key regret decision trees, >= %d cases per leaf, depth by source-grouped 4-fold "
-                           "cross-validation over %s" % (tree.MIN_LEAF, list(tree.DEPTHS)),
+                "regimes": "per key, the lower source-grouped 4-fold cross-validated regret of a regret decision "
+                           "tree (>= %d cases per leaf, depth from %s) and of the predefined intervals %s"
+                           % (tree.MIN_LEAF, list(tree.DEPTHS), SCHEMA),
                 "latency": "median of 3 kernel runs after 1 warm-up, HIP events"}
         if os.path.exists(args.eval):
             ev = load_records(args.eval)
@@ -221,7 +264,7 @@ def main():
             json.dump(doc, f, indent=1)
             f.write("\n")
         print(json.dumps(prov, indent=1))
-        print(json.dumps(doc["depths"]))
+        print(json.dumps(doc["partition"], indent=1))
         if os.path.exists(args.eval):
             print(json.dumps(regret_report_v2(regions, base, load_records(args.eval)), indent=1))
         return

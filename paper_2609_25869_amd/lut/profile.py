@@ -34,8 +34,17 @@ SEQ_LENS = [16384, 65536, 115200]
 BATCH_HEADS = [4, 24]
 FAMILIES = [("window", 0.05), ("window", 0.15), ("bernoulli", 0.03), ("bernoulli", 0.10), ("bernoulli", 0.30),
             ("topk", 0.12)]
-SPLIT_SEED = {"profile": 0, "eval": 1}
+SPLIT_SEED = {"profile": 0, "eval": 1, "wide": 2, "wide_eval": 3}
 FRAMES = 16
+
+# The wide splits draw, per request key, random combinations of a larger
+# grid: short and long sequences, few and many heads, twelve mask sources.
+WIDE_SEQ = [2048, 4096, 8192, 16384, 32768, 65536, 115200]
+WIDE_BH = [1, 2, 4, 8, 24]
+WIDE_SOURCES = [("window", 0.03), ("window", 0.08), ("window", 0.15), ("window", 0.30),
+                ("bernoulli", 0.02), ("bernoulli", 0.05), ("bernoulli", 0.10), ("bernoulli", 0.20),
+                ("bernoulli", 0.40), ("topk", 0.06), ("topk", 0.12), ("topk", 0.25)]
+WIDE_PER_KEY = {"wide": 96, "wide_eval": 48}
 
 
 def log(msg):
@@ -45,6 +54,15 @@ def log(msg):
 def corpus(split):
     """The deterministic case list of one split."""
     cases = []
+    if split in WIDE_PER_KEY:
+        import random
+        rng = random.Random(1000 + SPLIT_SEED[split])
+        for gi, geom in enumerate(GEOMETRIES):
+            for _ in range(WIDE_PER_KEY[split]):
+                fam, rho = rng.choice(WIDE_SOURCES)
+                cases.append(dict(id="%s-%d" % (split, len(cases)), geometry=list(geom), N=rng.choice(WIDE_SEQ),
+                                  bh=rng.choice(WIDE_BH), family=fam, rho=rho, seed=rng.randrange(1 << 30)))
+        return cases
     for gi, geom in enumerate(GEOMETRIES):
         for N in SEQ_LENS:
             for bh in BATCH_HEADS:

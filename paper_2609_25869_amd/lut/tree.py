@@ -185,36 +185,72 @@ def _select(leaves, case: Dict, base: int) -> int:
     return base
 
 
-def cv_depth(cases: Sequence[Dict], base: int, depths=DEPTHS, folds: int = 4, min_leaf: int = MIN_LEAF) -> int:
-    """Depth with the lowest held-out mean log regret; sources stay in one fold."""
+def _fold_of(cases: Sequence[Dict], folds: int) -> Dict:
     sources = sorted({source_of(c) for c in cases}, key=repr)
-    fold_of = {s: i % folds for i, s in enumerate(sources)}
+    return {s: i % folds for i, s in enumerate(sources)}
+
+
+def _cv_regret(cases: Sequence[Dict], base: int, build: Callable, folds: int = 4) -> float:
+    """Held-out mean log regret of the regimes `build(train_cases)` returns
+    (a list of (region, member cases)); sources stay in one fold."""
+    fold_of = _fold_of(cases, folds)
+    total, n = 0.0, 0
+    for f in range(folds):
+        train = [c for c in cases if fold_of[source_of(c)] != f]
+        test = [c for c in cases if fold_of[source_of(c)] == f]
+        if not train or not test:
+            continue
+        leaves = build(train)
+        for c in test:
+            lat = _lat(c)
+            p = _select(leaves, c, base)
+            if lat and p in lat:
+                total += math.log(lat[p] / min(lat.values()))
+                n += 1
+    return total / n if n else math.inf
+
+
+def grid_regions(cases: Sequence[Dict], schema) -> List[Tuple[Region, List[Dict]]]:
+    """Predefined intervals: the occupied cells of a bucket grid (Section 5.1),
+    as regions.  `schema` lists (feature, edges); features not in it are
+    unbounded."""
+    cells: Dict[Tuple, List[Dict]] = {}
+    edges_of = dict(schema)
+    for c in cases:
+        idx = []
+        for name in FEATURES:
+            edges = edges_of.get(name, [])
+            idx.append(sum(1 for e in edges if _ge(c["features"], name, e)))
+        cells.setdefault(tuple(idx), []).append(c)
+    out = []
+    for idx, members in sorted(cells.items()):
+        region = []
+        for name, i in zip(FEATURES, idx):
+            edges = list(edges_of.get(name, []))
+            region.append((edges[i - 1] if i > 0 else None, edges[i] if i < len(edges) else None))
+        out.append((region, members))
+    return out
+
+
+def cv_depth(cases: Sequence[Dict], base: int, depths=DEPTHS, folds: int = 4, min_leaf: int = MIN_LEAF) -> int:
+    """Depth with the lowest held-out mean log regret; ties go to the shallower tree."""
     best_d, best_r = depths[0], math.inf
     for d in depths:
-        total, n = 0.0, 0
-        for f in range(folds):
-            train = [c for c in cases if fold_of[source_of(c)] != f]
-            test = [c for c in cases if fold_of[source_of(c)] == f]
-            if not train or not test:
-                continue
-            leaves = grow(train, d, min_leaf)
-            for c in test:
-                lat = _lat(c)
-                if not lat:
-                    continue
-                p = _select(leaves, c, base)
-                if p in lat:
-                    total += math.log(lat[p] / min(lat.values()))
-                    n += 1
-        r = total / n if n else math.inf
+        r = _cv_regret(cases, base, lambda tr: grow(tr, d, min_leaf), folds)
         if r < best_r - 1e-12:
             best_d, best_r = d, r
     return best_d
 
 
 def compile_regions(records: Sequence[Dict], base_plan: Callable[[Tuple], int], min_leaf: int = MIN_LEAF,
-                    depths=DEPTHS) -> Dict[Tuple, Dict]:
-    """{key: {"depth": d, "regimes": [(region, ranking incl. base, n_cases)]}}."""
+                    depths=DEPTHS, grid_schema=None) -> Dict[Tuple, Dict]:
+    """{key: {"depth": d or None, "kind": "tree" | "grid", "cv_regret": r,
+    "regimes": [(region, ranking incl. base, n_cases)]}}.
+
+    Per key, the learned tree (depth by cross-validation) is compared, by the
+    same cross-validation, with the predefined intervals of `grid_schema`
+    when one is given, and the lower held-out regret wins (ties: the tree).
+    """
     by_key: Dict[Tuple, List[Dict]] = {}
     for r in records:
         if r["latency_ms"]:
@@ -223,12 +259,20 @@ def compile_regions(records: Sequence[Dict], base_plan: Callable[[Tuple], int], 
     for key, cases in sorted(by_key.items()):
         base = base_plan(key)
         d = cv_depth(cases, base, depths, min_leaf=min_leaf)
+        r_tree = _cv_regret(cases, base, lambda tr: grow(tr, d, min_leaf))
+        kind, leaves = "tree", grow(cases, d, min_leaf)
+        r_best = r_tree
+        if grid_schema is not None:
+            r_grid = _cv_regret(cases, base, lambda tr: grid_regions(tr, grid_schema))
+            if r_grid < r_tree - 1e-12:
+                kind, leaves, r_best = "grid", grid_regions(cases, grid_schema), r_grid
         regimes = []
-        for region, members in grow(cases, d, min_leaf):
+        for region, members in leaves:
             rk = ranking(members)
             if rk:
                 regimes.append((region, rk + [base], len(members)))
-        out[key] = {"depth": d, "regimes": regimes}
+        out[key] = {"depth": d if kind == "tree" else None, "kind": kind, "cv_regret": math.exp(r_best),
+                    "regimes": regimes}
     return out
 
 
