@@ -234,11 +234,79 @@ def kernel_ablations(pick, base_plan, catalog, records) -> Dict:
                                           "O1_vs_O0_wins_ties_losses": wtl}}
 
 
+def mapping_name(bq: int, bkv: int, tq: int, tkv: int) -> str:
+    """Section 4.2 mapping of logical blocks onto a physical tile."""
+    if tq == bq and tkv == bkv:
+        return "Direct"
+    if tq >= bq and tkv >= bkv:
+        return "Coarsened"
+    if tq <= bq and tkv <= bkv:
+        return "Refined"
+    return "mixed"
+
+
+def mapping_census(catalog, records) -> Dict[str, Dict[str, float]]:
+    """Per key, the share of cases whose fastest measured plan uses each mapping."""
+    tile = {e["id"]: (e["tq"], e["tkv"]) for e in catalog}
+    out: Dict[str, Dict[str, int]] = {}
+    for r in records:
+        lat = {int(p): t for p, t in r["latency_ms"].items()}
+        if not lat:
+            continue
+        bq, bkv = r["key"][:2]
+        best = min(lat, key=lat.get)
+        kind = mapping_name(bq, bkv, *tile[best])
+        c = out.setdefault("%d:%d" % (bq, bkv), {})
+        c[kind] = c.get(kind, 0) + 1
+    return {k: {m: n / sum(v.values()) for m, n in sorted(v.items())} for k, v in sorted(out.items())}
+
+
+def write_report(path: str, table, base, catalog, prof_recs, eval_recs) -> None:
+    """Markdown summary of the shipped table: regret, census, ablations."""
+    pick = lambda r: table.get(tuple(r["key"]), {}).get(bucket(r["features"], SCHEMA), [base(tuple(r["key"]))])
+    lines = ["# gfx950 plan table: selection quality on MI355X", "",
+             "Generated by `python -m paper_2609_25869_amd.lut.compile --report` from the committed profiling "
+             "records (`gfx950_profile.jsonl`, table built from it; `gfx950_eval.jsonl`, held-out cases of the same "
+             "generators with other seeds).  Latencies are kernel times (median of 3 after 1 warm-up, HIP events).",
+             "", "## Selector regret (selected / fastest measured latency per case)", "",
+             "| cases | GM | P95 | P99 | max | within 3% |", "|---|---:|---:|---:|---:|---:|"]
+    for name, recs in (("profile (in-sample)", prof_recs), ("eval (held-out)", eval_recs)):
+        a = regret_report(table, SCHEMA, base, recs)["all"]
+        lines.append("| %s: %d | %.4f | %.4f | %.4f | %.4f | %.1f%% |" % (
+            name, a["cases"], a["gm"], a["p95"], a["p99"], a["max"], 100 * a["within_3pct"]))
+    lines += ["", "Held-out regret per request key (B_Q:B_KV):", "",
+              "| key | cases | GM | P95 | max |", "|---|---:|---:|---:|---:|"]
+    for k, a in regret_report(table, SCHEMA, base, eval_recs)["per_key"].items():
+        lines.append("| %s | %d | %.4f | %.4f | %.4f |" % (k, a["cases"], a["gm"], a["p95"], a["max"]))
+    lines += ["", "## Mapping census: share of held-out cases whose fastest plan uses each mapping (Section 4.2)", "",
+              "| key | Direct | Coarsened | Refined | mixed |", "|---|---:|---:|---:|---:|"]
+    for k, c in mapping_census(catalog, eval_recs).items():
+        lines.append("| %s | %s |" % (k, " | ".join("%.0f%%" % (100 * c.get(m, 0))
+                                                   for m in ("Direct", "Coarsened", "Refined", "mixed"))))
+    ab = kernel_ablations(pick, base, catalog, eval_recs)
+    o = ab["organization_at_base_tile"]
+    lines += ["", "## Kernel-time ablations on the held-out cases (paired-case geometric means)", "",
+              "| variant | speedup over A0 (Direct) |", "|---|---:|",
+              "| A1: fastest measured eligible plan (exhaustive search) | %.3f |" % ab["kernel_speedup_over_A0"]["A1_exhaustive"],
+              "| A2: plan-table selection | %.3f |" % ab["kernel_speedup_over_A0"]["A2_table"],
+              "", "A2 / A1 kernel time: %.4f." % ab["A2_regret_vs_A1"], "",
+              "Task organization at the base tile (only the Split-K factor varies):", "",
+              "| variant | speedup over O0 | regret vs O2 |", "|---|---:|---:|",
+              "| O0: base organization (no split) | 1.000 | %.4f |" % o["O0_regret_vs_O2"],
+              "| O1: table's first plan with that tile | %.3f | %.4f |" % (o["O1_speedup_over_O0"], o["O1_regret_vs_O2"]),
+              "| O2: fastest measured organization | %.3f | 1.0000 |" % o["O2_speedup_over_O0"],
+              "", "O1 against O0 with a 3%% tie band: %d wins, %d ties, %d losses." % tuple(o["O1_vs_O0_wins_ties_losses"]),
+              ""]
+    with open(path, "w") as f:
+        f.write("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--profile", default=os.path.join(HERE, "gfx950_profile.jsonl"))
     ap.add_argument("--eval", default=os.path.join(HERE, "gfx950_eval.jsonl"))
     ap.add_argument("--out", default=None)
+    ap.add_argument("--report", action="store_true", help="also write gfx950_report.md beside the table")
     ap.add_argument("--tree", action="store_true",
                     help="learn the regimes with per-key decision trees (version-2 artifact)")
     args = ap.parse_args()
@@ -286,6 +354,9 @@ def main():
     print(json.dumps(prov, indent=1))
     if os.path.exists(args.eval):
         print(json.dumps(regret_report(table, SCHEMA, base, load_records(args.eval)), indent=1))
+        if args.report:
+            write_report(os.path.join(HERE, "gfx950_report.md"), table, base, bsa.catalog(), recs,
+                         load_records(args.eval))
 
 
 if __name__ == "__main__":
