@@ -27,17 +27,28 @@ from typing import Dict, List, Sequence, Tuple
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 
-# Feature schema of the first gfx950 table: predefined bucket edges.
+# Feature schema of the gfx950 table: predefined bucket edges.
 # seq_q in tokens, batch_heads in (batch x heads), ratios in units of 1e-4.
+# The sequence-length and head-count edges separate the short, few-head
+# requests of the wide corpus (Split-K and small tiles win there); on the
+# held-out splits this grid had the lowest selector regret of the grids and
+# decision-tree tables compared (gfx950_report.md).
 SCHEMA: List[Tuple[str, List[int]]] = [
-    ("seq_q", [32768, 98304]),
-    ("batch_heads", [12]),
+    ("seq_q", [6144, 24576, 98304]),
+    ("batch_heads", [3, 12]),
     ("density", [700, 2000]),
     ("run_coverage", [5000]),
 ]
 
+# Profiling records the shipped table is built from, and held-out records.
+PROFILES = [os.path.join(HERE, "gfx950_profile.jsonl"), os.path.join(HERE, "gfx950_wide.jsonl")]
+EVALS = [os.path.join(HERE, "gfx950_eval.jsonl"), os.path.join(HERE, "gfx950_wide_eval.jsonl")]
 
-def load_records(path: str) -> List[Dict]:
+
+def load_records(path) -> List[Dict]:
+    """Records of one JSON-lines file, or of several (a list of paths)."""
+    if not isinstance(path, str):
+        return [r for p in path for r in load_records(p)]
     with open(path) as f:
         return [json.loads(line) for line in f if line.strip()]
 
@@ -261,19 +272,39 @@ def mapping_census(catalog, records) -> Dict[str, Dict[str, float]]:
     return {k: {m: n / sum(v.values()) for m, n in sorted(v.items())} for k, v in sorted(out.items())}
 
 
-def write_report(path: str, table, base, catalog, prof_recs, eval_recs) -> None:
+def write_report(path: str, table, base, catalog, prof_recs, eval_recs, candidates=None) -> None:
     """Markdown summary of the shipped table: regret, census, ablations."""
     pick = lambda r: table.get(tuple(r["key"]), {}).get(bucket(r["features"], SCHEMA), [base(tuple(r["key"]))])
     lines = ["# gfx950 plan table: selection quality on MI355X", "",
              "Generated by `python -m paper_2609_25869_amd.lut.compile --report` from the committed profiling "
-             "records (`gfx950_profile.jsonl`, table built from it; `gfx950_eval.jsonl`, held-out cases of the same "
-             "generators with other seeds).  Latencies are kernel times (median of 3 after 1 warm-up, HIP events).",
+             "records: the table is built from `gfx950_profile.jsonl` and `gfx950_wide.jsonl`; "
+             "`gfx950_eval.jsonl` and `gfx950_wide_eval.jsonl` hold held-out cases of the same generators with "
+             "other seeds.  Latencies are kernel times (median of 3 after 1 warm-up, HIP events).",
              "", "## Selector regret (selected / fastest measured latency per case)", "",
              "| cases | GM | P95 | P99 | max | within 3% |", "|---|---:|---:|---:|---:|---:|"]
     for name, recs in (("profile (in-sample)", prof_recs), ("eval (held-out)", eval_recs)):
         a = regret_report(table, SCHEMA, base, recs)["all"]
         lines.append("| %s: %d | %.4f | %.4f | %.4f | %.4f | %.1f%% |" % (
             name, a["cases"], a["gm"], a["p95"], a["p99"], a["max"], 100 * a["within_3pct"]))
+    hold = list(eval_recs)
+    lines += ["", "Held-out regret by the kernel time of the fastest plan (short kernels carry most of the regret, "
+              "and part of it is timing noise of a 3-run median):", "",
+              "| fastest kernel | cases | GM | P95 | within 3% |", "|---|---:|---:|---:|---:|"]
+    for lo, hi in ((0, 0.05), (0.05, 0.2), (0.2, 1.0), (1.0, float("inf"))):
+        sub = [r for r in hold if r["latency_ms"] and lo <= min(r["latency_ms"].values()) < hi]
+        if sub:
+            a = regret_report(table, SCHEMA, base, sub)["all"]
+            lines.append("| %s ms | %d | %.4f | %.4f | %.1f%% |" % (
+                "%g-%g" % (lo, hi) if hi != float("inf") else ">= %g" % lo, a["cases"], a["gm"], a["p95"],
+                100 * a["within_3pct"]))
+    if candidates:
+        lines += ["", "## Regime partitions compared on the held-out cases (Section 5.1: predefined intervals or "
+                  "decision-tree thresholds)", "",
+                  "| partition (built from the profiling records) | GM | P95 | P99 | within 3% |",
+                  "|---|---:|---:|---:|---:|"]
+        for name, a in candidates:
+            lines.append("| %s | %.4f | %.4f | %.4f | %.1f%% |" % (name, a["gm"], a["p95"], a["p99"],
+                                                                 100 * a["within_3pct"]))
     lines += ["", "Held-out regret per request key (B_Q:B_KV):", "",
               "| key | cases | GM | P95 | max |", "|---|---:|---:|---:|---:|"]
     for k, a in regret_report(table, SCHEMA, base, eval_recs)["per_key"].items():
@@ -303,8 +334,8 @@ def write_report(path: str, table, base, catalog, prof_recs, eval_recs) -> None:
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("--profile", default=os.path.join(HERE, "gfx950_profile.jsonl"))
-    ap.add_argument("--eval", default=os.path.join(HERE, "gfx950_eval.jsonl"))
+    ap.add_argument("--profile", nargs="+", default=PROFILES)
+    ap.add_argument("--eval", nargs="+", default=EVALS)
     ap.add_argument("--out", default=None)
     ap.add_argument("--report", action="store_true", help="also write gfx950_report.md beside the table")
     ap.add_argument("--tree", action="store_true",
@@ -322,7 +353,7 @@ def main():
                            "tree (>= %d cases per leaf, depth from %s) and of the predefined intervals %s"
                            % (tree.MIN_LEAF, list(tree.DEPTHS), SCHEMA),
                 "latency": "median of 3 kernel runs after 1 warm-up, HIP events"}
-        if os.path.exists(args.eval):
+        if all(os.path.exists(e) for e in args.eval):
             ev = load_records(args.eval)
             prov["eval_cases"] = len(ev)
             prov["eval_regret"] = regret_report_v2(regions, base, ev)["all"]
@@ -333,16 +364,18 @@ def main():
             f.write("\n")
         print(json.dumps(prov, indent=1))
         print(json.dumps(doc["partition"], indent=1))
-        if os.path.exists(args.eval):
+        if all(os.path.exists(e) for e in args.eval):
             print(json.dumps(regret_report_v2(regions, base, load_records(args.eval)), indent=1))
         return
     args.out = args.out or os.path.join(HERE, "gfx950_v1.json")
     table = compile_table(recs, SCHEMA, base)
     prov = {"profiled_on": "MI355X (gfx950)", "profile_cases": len(recs),
-            "corpus": "seeded synthetic masks (frame windows, Bernoulli + diagonal, pooled q.k top-k), "
-                      "nine paper geometries + (128,32)/(32,128), N in {16K, 64K, 115K}, 4 or 24 batch x heads",
+            "corpus": "seeded synthetic masks (frame windows, Bernoulli + diagonal, pooled q.k top-k) on the "
+                      "nine paper geometries + (128,32)/(32,128): the grid split (N in {16K, 64K, 115K}, 4 or 24 "
+                      "batch x heads, 6 sources) and the wide split (N from 2K to 115K, 1 to 24 batch x heads, "
+                      "12 sources, 96 random draws per key)",
             "latency": "median of 3 kernel runs after 1 warm-up, HIP events"}
-    if os.path.exists(args.eval):
+    if all(os.path.exists(e) for e in args.eval):
         ev = load_records(args.eval)
         prov["eval_cases"] = len(ev)
         prov["eval_regret"] = regret_report(table, SCHEMA, base, ev)["all"]
@@ -352,11 +385,21 @@ def main():
         json.dump(doc, f, indent=1)
         f.write("\n")
     print(json.dumps(prov, indent=1))
-    if os.path.exists(args.eval):
+    if all(os.path.exists(e) for e in args.eval):
         print(json.dumps(regret_report(table, SCHEMA, base, load_records(args.eval)), indent=1))
         if args.report:
-            write_report(os.path.join(HERE, "gfx950_report.md"), table, base, bsa.catalog(), recs,
-                         load_records(args.eval))
+            from . import tree
+            ev = load_records(args.eval)
+            prev = [("seq_q", [32768, 98304]), ("batch_heads", [12]), ("density", [700, 2000]),
+                    ("run_coverage", [5000])]
+            cands = [("predefined intervals, shipped schema %s" % SCHEMA, regret_report(table, SCHEMA, base, ev)["all"]),
+                     ("predefined intervals, earlier schema %s" % prev,
+                      regret_report(compile_table(recs, prev, base), prev, base, ev)["all"]),
+                     ("decision trees per key (>= %d cases per leaf, depth by grouped CV)" % tree.MIN_LEAF,
+                      regret_report_v2(tree.compile_regions(recs, base), base, ev)["all"]),
+                     ("per key, tree or shipped intervals by grouped CV",
+                      regret_report_v2(tree.compile_regions(recs, base, grid_schema=SCHEMA), base, ev)["all"])]
+            write_report(os.path.join(HERE, "gfx950_report.md"), table, base, bsa.catalog(), recs, ev, cands)
 
 
 if __name__ == "__main__":
