@@ -103,3 +103,37 @@ def test_held_out_selection_regret():
     long = [r for r in held if min(r["latency_ms"].values()) >= 1.0]
     rep_long = lutc.regret_report(table, lutc.SCHEMA, base, long)["all"]
     assert rep_long["cases"] >= 150 and rep_long["gm"] < 1.02
+
+
+def test_kernel_ablations_on_constructed_records():
+    """A0 = base plan, A1 = fastest, A2 = the pick; O-variants keep the base tile."""
+    cat = bsa.catalog()
+    key = [64, 64, 0, 128]
+    b = base(tuple(key))                         # Direct (64,64), split 1
+    same_tile = [e["id"] for e in cat if (e["tq"], e["tkv"]) == (64, 64) and e["id"] != b]
+    other = [e["id"] for e in cat if (e["tq"], e["tkv"]) != (64, 64)][0]
+    recs = [{"key": key, "features": {}, "latency_ms": {str(b): 2.0, str(same_tile[0]): 1.6, str(other): 1.0}}]
+    out = lutc.kernel_ablations(lambda r: [same_tile[0]], base, cat, recs)
+    assert math.isclose(out["kernel_speedup_over_A0"]["A1_exhaustive"], 2.0)
+    assert math.isclose(out["kernel_speedup_over_A0"]["A2_table"], 2.0 / 1.6)
+    o = out["organization_at_base_tile"]
+    assert math.isclose(o["O1_speedup_over_O0"], 2.0 / 1.6) and math.isclose(o["O1_regret_vs_O2"], 1.0)
+    assert o["O1_vs_O0_wins_ties_losses"] == [1, 0, 0]
+
+
+def test_mapping_names_follow_section_4_2():
+    assert lutc.mapping_name(64, 64, 64, 64) == "Direct"
+    assert lutc.mapping_name(16, 16, 64, 32) == "Coarsened"
+    assert lutc.mapping_name(128, 128, 128, 64) == "Refined"
+    assert lutc.mapping_name(32, 128, 64, 32) == "mixed"
+
+
+def test_request_ablation_summary():
+    from paper_2609_25869_amd.lut import ablation
+    recs = [{"plans": {"A0": 4, "A1": 8, "A2": 8},
+             "request_ms": {"A0": [2.0, 2.0, 2.0, 2.0], "A1": [40.0, 1.5, 1.5, 1.5], "A2": [1.6, 1.0, 1.0, 1.0]},
+             "kernel_ms": {"A0": 1.8, "A1": 1.2, "A2": 1.2}}]
+    s = ablation.summarize(recs)
+    assert math.isclose(s["cold"]["A1/A2"], 40.0 / 1.6) and math.isclose(s["warm"]["A0/A2"], 2.0)
+    assert math.isclose(s["amortized"]["A0/A1"], 2.0 / ((40 + 4.5) / 4))
+    assert math.isclose(s["kernel"]["A0/A2"], 1.5) and s["same_plan_as_A1"] == 1.0
