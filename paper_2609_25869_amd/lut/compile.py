@@ -328,6 +328,23 @@ def write_report(path: str, table, base, catalog, prof_recs, eval_recs, candidat
               "| O2: fastest measured organization | %.3f | 1.0000 |" % o["O2_speedup_over_O0"],
               "", "O1 against O0 with a 3%% tie band: %d wins, %d ties, %d losses." % tuple(o["O1_vs_O0_wins_ties_losses"]),
               ""]
+    abl = os.path.join(HERE, "gfx950_ablation.jsonl")
+    if os.path.exists(abl):
+        from . import ablation
+        recs = load_records(abl)
+        sm = ablation.summarize(recs)
+        lines += ["## Complete requests: A0 Direct, A1 exhaustive online search, A2 plan table", "",
+                  "`gfx950_ablation.jsonl`, written by `python -m paper_2609_25869_amd.lut.ablation --split eval "
+                  "--every 4` (every fourth held-out case of the grid split, %d cases; "
+                  "pass 1 is the cold unique request, passes 2-4 warm exact repeats, amortized = mean of the four). "
+                  "Paired-case geometric means of latency ratios:" % sm["cases"], "",
+                  "| population | T_A0 / T_A1 | T_A1 / T_A2 | T_A0 / T_A2 |", "|---|---:|---:|---:|"]
+        for pop in ("cold", "warm", "amortized"):
+            lines.append("| %s | %.3f | %.2f | %.3f |" % (pop, sm[pop]["A0/A1"], sm[pop]["A1/A2"], sm[pop]["A0/A2"]))
+        lines += ["", "Kernel time of the plan each variant executes: A0 / A1 %.3f, A0 / A2 %.3f, A2 / A1 %.4f; "
+                  "A2 picks A1's plan in %.0f%% of the cases." % (sm["kernel"]["A0/A1"], sm["kernel"]["A0/A2"],
+                                                                  sm["kernel"]["A2/A1"], 100 * sm["same_plan_as_A1"]),
+                  ""]
     with open(path, "w") as f:
         f.write("\n".join(lines))
 
