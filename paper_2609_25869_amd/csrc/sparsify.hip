@@ -40,8 +40,17 @@ __global__ __launch_bounds__(128) void block_mean_kernel(const uint16_t* x, int6
   const int c = threadIdx.x;
   const uint16_t* p = x + b * s0 + h * s1 + c;
   const int32_t r0 = i * blk, r1 = min(n, r0 + blk);
+  // rows in increasing order; eight loads go out before their additions
   double s = 0.0;
-  for (int32_t r = r0; r < r1; ++r) s += bf16_to_f64(p[(int64_t)r * s2]);
+  int32_t r = r0;
+  for (; r + 8 <= r1; r += 8) {
+    double v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = bf16_to_f64(p[(int64_t)(r + j) * s2]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s += v[j];
+  }
+  for (; r < r1; ++r) s += bf16_to_f64(p[(int64_t)r * s2]);
   out[w * kHeadDim + c] = s / (double)(r1 - r0);
 }
 
@@ -106,6 +115,17 @@ __device__ inline uint64_t order_key(double x) {
   return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ inline uint32_t wave_inclusive_scan(uint32_t x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
 __global__ __launch_bounds__(256) void topk_select_kernel(const double* scores, int32_t nqb, int32_t nkb, int32_t k,
                                                           int32_t diagonal, int32_t nq, int32_t nkv, int32_t bq,
                                                           int32_t bkv, int32_t bh0, uint8_t* mask) {
@@ -137,14 +157,31 @@ __global__ __launch_bounds__(256) void topk_select_kernel(const double* scores, 
         if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255], 1u);
       }
       __syncthreads();
-      if (tid == 0) {
-        int32_t above = 0, d = 255;
-        for (; d > 0; --d) {
-          if (above + (int32_t)hist[d] >= remaining) break;
-          above += (int32_t)hist[d];
+      if (tid < 64) {
+        // digit d of the sought key: the largest d whose keys, counted from
+        // digit 255 down to d, reach `remaining` (d = 0 if none does before).
+        // Lane l holds digits 255-4l .. 252-4l.
+        uint32_t cnt[4], local = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          cnt[j] = hist[255 - 4 * tid - j];
+          local += cnt[j];
         }
-        s_remaining = remaining - above;
-        s_prefix = prefix | ((uint64_t)d << shift);
+        const uint32_t incl = wave_inclusive_scan(local);
+        const uint64_t reach = __ballot(incl >= (uint32_t)remaining || tid == 63);
+        const int first = __builtin_ctzll(reach);
+        if (tid == first) {
+          int32_t above = (int32_t)(incl - local);
+          int d = 255 - 4 * tid;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            if (d == 0 || above + (int32_t)cnt[j] >= remaining) break;
+            above += (int32_t)cnt[j];
+            --d;
+          }
+          s_remaining = remaining - above;
+          s_prefix = prefix | ((uint64_t)d << shift);
+        }
       }
       __syncthreads();
       remaining = s_remaining;
@@ -159,12 +196,19 @@ __global__ __launch_bounds__(256) void topk_select_kernel(const double* scores, 
     for (int32_t kb = c0; kb < c1; ++kb) ties += keys[kb] == prefix;
     chunk_ties[tid] = ties;
     __syncthreads();
-    if (tid == 0) {
-      uint32_t run = 0;
-      for (int i = 0; i < 256; ++i) {
-        const uint32_t t = chunk_ties[i];
-        chunk_ties[i] = run;
-        run += t;
+    if (tid < 64) {
+      // exclusive prefix over the 256 chunks, four per lane
+      uint32_t t[4], local = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        t[j] = chunk_ties[4 * tid + j];
+        local += t[j];
+      }
+      uint32_t run = wave_inclusive_scan(local) - local;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        chunk_ties[4 * tid + j] = run;
+        run += t[j];
       }
     }
     __syncthreads();
