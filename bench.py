@@ -189,9 +189,13 @@ def main():
 
     sp_ms = []
 
-    def request():
+    def evict_caches():
+        # outside the request: the write and its completion precede the timer
         if flush is not None:
             flush.fill_(1)
+        torch.cuda.synchronize()
+
+    def request():
         if topk is not None:
             s0 = torch.cuda.Event(enable_timing=True)
             s1 = torch.cuda.Event(enable_timing=True)
@@ -210,14 +214,16 @@ def main():
         return p, e0, e1
 
     for _ in range(args.warmup):
+        evict_caches()
         p, _, _ = request()
         torch.cuda.synchronize()
         p.destroy()
 
-    torch.cuda.synchronize()
+    # K timed steps, each a complete request between two synchronisations;
+    # the timed region is their sum
     req_ms, kern = [], []
-    t_start = time.perf_counter()
     for _ in range(args.steps):
+        evict_caches()
         t1 = time.perf_counter()
         p, e0, e1 = request()
         stream.synchronize()
@@ -226,7 +232,7 @@ def main():
         if _ < args.steps - 1:
             p.destroy()
     torch.cuda.synchronize()
-    total_s = time.perf_counter() - t_start
+    total_s = sum(req_ms) * 1e-3
     kernel_ms = [a.elapsed_time(b) for a, b in kern]
     info = [p.info(s) for s in range(p.num_segments())]
 

@@ -174,6 +174,8 @@ __global__ void zero_i64(int64_t* out) {
 }
 
 // ---------------------------------------------------------------------------
+constexpr int kMapBatch = 16;
+
 // Physical mapping of one geometry segment (Section 4.2): tile (pq, pk) is
 // active iff one of its member logical blocks is; bit a*gkv + c records
 // member (a, c) for Coarsened tiles.
@@ -199,6 +201,34 @@ __global__ __launch_bounds__(256) void map_rows_kernel(MapArgs a) {
   }
   const int64_t out_base = kFill ? a.tile_ptr[rp] : 0;
   int64_t n = 0;
+  if (a.gq == 1 && a.gkv == 1) {
+    // Direct and Refined: one member per tile, the block (qb0, pk / rkv).
+    // Every byte load of kMapBatch steps of 64 tiles is issued (from a
+    // clamped address, so none sits behind a branch) before the first
+    // ballot: a row costs one memory latency per 1024 tiles.
+    const uint8_t* row = mh + (int64_t)qb0 * a.nkb;
+    for (int p00 = 0; p00 < a.npk; p00 += 64 * kMapBatch) {
+      uint8_t v[kMapBatch];
+#pragma unroll
+      for (int j = 0; j < kMapBatch; ++j) v[j] = row[min(p00 + 64 * j + lane, a.npk - 1) / a.rkv];
+      bool act[kMapBatch];
+#pragma unroll
+      for (int j = 0; j < kMapBatch; ++j) act[j] = (p00 + 64 * j + lane < a.npk) && v[j] != 0;
+#pragma unroll
+      for (int j = 0; j < kMapBatch; ++j) {
+        if (p00 + 64 * j >= a.npk) break;
+        const uint64_t ball = __ballot(act[j]);
+        if (kFill && act[j]) {
+          const int64_t pos = out_base + n + __popcll(ball & lanes_below(lane));
+          a.tile_kv[pos] = p00 + 64 * j + lane;
+          if (a.member) a.member[pos] = 1ull;
+        }
+        n += __popcll(ball);
+      }
+    }
+    if (!kFill && lane == 0) a.counts[rp] = (int32_t)n;
+    return;
+  }
   for (int p0 = 0; p0 < a.npk; p0 += 64) {
     const int pk = p0 + lane;
     uint64_t bits = 0;
