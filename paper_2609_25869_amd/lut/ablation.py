@@ -39,15 +39,7 @@ def _time_request(torch, stream, fn):
 
 
 def _kernel_ms(torch, stream, bsa, p, q, k, v, o, reps=3):
-    ts = []
-    for _ in range(reps + 1):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        bsa.forward(p, q, k, v, o, None, stream=stream)
-        e1.record(stream)
-        e1.synchronize()
-        ts.append(e0.elapsed_time(e1))
-    return sorted(ts[1:])[len(ts[1:]) // 2]
+    return prof.kernel_time(torch, stream, lambda: bsa.forward(p, q, k, v, o, None, stream=stream), reps)
 
 
 def run_case(torch, bsa, case):

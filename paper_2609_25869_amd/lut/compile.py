@@ -279,7 +279,9 @@ def write_report(path: str, table, base, catalog, prof_recs, eval_recs, candidat
              "Generated by `python -m paper_2609_25869_amd.lut.compile --report` from the committed profiling "
              "records: the table is built from `gfx950_profile.jsonl` and `gfx950_wide.jsonl`; "
              "`gfx950_eval.jsonl` and `gfx950_wide_eval.jsonl` hold held-out cases of the same generators with "
-             "other seeds.  Latencies are kernel times (median of 3 after 1 warm-up, HIP events).",
+             "other seeds.  Latencies are kernel times: the median of 3 timed batches after 1 warm-up launch, "
+             "where a launch shorter than 1 ms is timed in batches of back-to-back launches of about 1 ms "
+             "(HIP events around each batch).",
              "", "## Selector regret (selected / fastest measured latency per case)", "",
              "| cases | GM | P95 | P99 | max | within 3% |", "|---|---:|---:|---:|---:|---:|"]
     for name, recs in (("profile (in-sample)", prof_recs), ("eval (held-out)", eval_recs)):
@@ -287,8 +289,8 @@ def write_report(path: str, table, base, catalog, prof_recs, eval_recs, candidat
         lines.append("| %s: %d | %.4f | %.4f | %.4f | %.4f | %.1f%% |" % (
             name, a["cases"], a["gm"], a["p95"], a["p99"], a["max"], 100 * a["within_3pct"]))
     hold = list(eval_recs)
-    lines += ["", "Held-out regret by the kernel time of the fastest plan (short kernels carry most of the regret, "
-              "and part of it is timing noise of a 3-run median):", "",
+    lines += ["", "Held-out regret by the kernel time of the fastest plan (short kernels carry most of the regret: "
+              "there a plan's launch geometry matters most and the regimes are coarsest):", "",
               "| fastest kernel | cases | GM | P95 | within 3% |", "|---|---:|---:|---:|---:|"]
     for lo, hi in ((0, 0.05), (0.05, 0.2), (0.2, 1.0), (1.0, float("inf"))):
         sub = [r for r in hold if r["latency_ms"] and lo <= min(r["latency_ms"].values()) < hi]
@@ -369,7 +371,7 @@ def main():
                 "regimes": "per key, the lower source-grouped 4-fold cross-validated regret of a regret decision "
                            "tree (>= %d cases per leaf, depth from %s) and of the predefined intervals %s"
                            % (tree.MIN_LEAF, list(tree.DEPTHS), SCHEMA),
-                "latency": "median of 3 kernel runs after 1 warm-up, HIP events"}
+                "latency": "median of 3 timed batches after 1 warm-up launch; launches under 1 ms timed as back-to-back batches of about 1 ms (HIP events)"}
         if all(os.path.exists(e) for e in args.eval):
             ev = load_records(args.eval)
             prov["eval_cases"] = len(ev)
@@ -391,7 +393,7 @@ def main():
                       "nine paper geometries + (128,32)/(32,128): the grid split (N in {16K, 64K, 115K}, 4 or 24 "
                       "batch x heads, 6 sources) and the wide split (N from 2K to 115K, 1 to 24 batch x heads, "
                       "12 sources, 96 random draws per key)",
-            "latency": "median of 3 kernel runs after 1 warm-up, HIP events"}
+            "latency": "median of 3 timed batches after 1 warm-up launch; launches under 1 ms timed as back-to-back batches of about 1 ms (HIP events)"}
     if all(os.path.exists(e) for e in args.eval):
         ev = load_records(args.eval)
         prov["eval_cases"] = len(ev)

@@ -2,8 +2,10 @@
 
 Runs every eligible catalog plan on a corpus of seeded synthetic masks and
 records, per case, the request key, the regime features the online path will
-see (the library's own mask statistics) and the median kernel latency of each
-plan whose output passed validation.  The output is one JSON line per case;
+see (the library's own mask statistics) and the kernel latency of each plan
+whose output passed validation (``kernel_time``: the median of three timed
+batches; launches shorter than a millisecond are timed as batches of
+back-to-back launches, so event and launch jitter average out).  The output is one JSON line per case;
 ``compile.py`` turns those lines into the plan table.
 
 Validation: every plan's output must be finite and agree with the key's base
@@ -115,6 +117,29 @@ def make_mask(torch, case, q, k):
     return out
 
 
+BATCH_MS = 1.0   # a timed batch of short launches lasts about this long
+MAX_BATCH = 64
+
+
+def kernel_time(torch, stream, launch, reps=3):
+    """Kernel time of one launch (ms): one warm-up launch sizes a batch of
+    back-to-back launches lasting about BATCH_MS; the median over `reps`
+    batches of the mean per launch (HIP events around each batch).  Kernels
+    longer than BATCH_MS are timed one launch per batch."""
+    def batch(n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(n):
+            launch()
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) / n
+    first = batch(1)
+    n = max(1, min(MAX_BATCH, int(math.ceil(BATCH_MS / max(first, 1e-3)))))
+    ts = sorted(batch(n) for _ in range(reps))
+    return ts[len(ts) // 2]
+
+
 def profile_case(torch, bsa, case, reps=3):
     bq, bkv = case["geometry"]
     N, bh = case["N"], case["bh"]
@@ -146,15 +171,7 @@ def profile_case(torch, bsa, case, reps=3):
             info = p.info(0)
             feats = {"seq_q": N, "seq_kv": N, "batch_heads": bh, "nnz": info["nnz"], "blocks": info["blocks"],
                      "run_blocks": info["run_blocks"]}
-        ts = []
-        for r in range(reps + 1):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            bsa.forward(p, q, k, v, o, None, stream=stream)
-            e1.record(stream)
-            e1.synchronize()
-            if r > 0:
-                ts.append(e0.elapsed_time(e1))
+        t = kernel_time(torch, stream, lambda: bsa.forward(p, q, k, v, o, None, stream=stream), reps)
         p.destroy()
         ok = bool(torch.isfinite(o).all().item())
         if ok and ref is None:
@@ -162,7 +179,7 @@ def profile_case(torch, bsa, case, reps=3):
         elif ok:
             ok = float((o.float() - ref.float()).abs().max().item()) <= 2e-2
         if ok:
-            lat[pid] = sorted(ts)[len(ts) // 2]
+            lat[pid] = t
         else:
             invalid.append(pid)
     del q, k, v, o, mask, ref
