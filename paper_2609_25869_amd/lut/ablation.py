@@ -15,6 +15,13 @@ already on the device.  Pass 1 is the cold unique request, passes 2-4 the
 warm exact repeats, and the amortized latency averages all four.  The
 kernel columns are the execution time of the plan each variant ends with.
 
+Dispatch overhead (the measurement of Table 7, Section 6): per case, the
+wall time of A2's preparation alone (bsa_plan: the mask state on the device,
+the one statistics copy, lookup and eligibility, the metadata launches;
+stream synchronised), PASSES times, and of the host lookup and eligibility
+alone (bsa_select_plan on the same statistics, through the Python binding),
+SELECT_CALLS times.
+
     python -m paper_2609_25869_amd.lut.ablation --out OUT.jsonl [--split eval] [--every 3] [--budget S]
 """
 from __future__ import annotations
@@ -28,6 +35,7 @@ import time
 from . import profile as prof
 
 PASSES = 4
+SELECT_CALLS = 200
 
 
 def _time_request(torch, stream, fn):
@@ -118,6 +126,24 @@ def run_case(torch, bsa, case):
         a2.append(ms)
     chosen = p2.info(0)["plan_id"]
 
+    # dispatch overhead
+    plan_ms = []
+    for _ in range(PASSES):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        pp = prepare(-1)
+        stream.synchronize()
+        plan_ms.append((time.perf_counter() - t0) * 1e3)
+        pp.destroy()
+    inf = p2.info(0)
+    z = bsa.regime_query(bq, bkv, bh, N, N, inf["nnz"], inf["blocks"], inf["run_blocks"])
+    sel_us = []
+    for _ in range(SELECT_CALLS):
+        t0 = time.perf_counter_ns()
+        bsa.select_plan(z, shapes)
+        sel_us.append((time.perf_counter_ns() - t0) / 1e3)
+    sel_us.sort()
+
     pa0, pa1 = prepare(base), prepare(winner)
     rec.update({
         "plans": {"A0": base, "A1": winner, "A2": chosen},
@@ -126,6 +152,8 @@ def run_case(torch, bsa, case):
                       "A1": _kernel_ms(torch, stream, bsa, pa1, q, k, v, o),
                       "A2": _kernel_ms(torch, stream, bsa, p2, q, k, v, o)},
         "eligible": len(eligible),
+        "plan_ms": plan_ms,
+        "select_us": {"mean": sum(sel_us) / len(sel_us), "p95": sel_us[int(0.95 * (len(sel_us) - 1))]},
     })
     for p in (pa0, pa1, p2):
         p.destroy()
@@ -154,7 +182,23 @@ def summarize(records):
                      "A0/A2": gm([r["kernel_ms"]["A0"] / r["kernel_ms"]["A2"] for r in records]),
                      "A2/A1": gm([r["kernel_ms"]["A2"] / r["kernel_ms"]["A1"] for r in records])}
     out["same_plan_as_A1"] = sum(r["plans"]["A1"] == r["plans"]["A2"] for r in records) / max(1, len(records))
+    out["dispatch"] = dispatch_summary(records)
     return out
+
+
+def _mean_p95(xs):
+    xs = sorted(xs)
+    return {"n": len(xs), "mean": sum(xs) / len(xs), "p95": xs[int(0.95 * (len(xs) - 1))]} if xs else None
+
+
+def dispatch_summary(records, key=None):
+    """Mean and P95 over requests of bsa_plan (first pass, later passes) and
+    of the host lookup and eligibility, for all cases or one key."""
+    recs = [r for r in records if "plan_ms" in r and (key is None or tuple(r["key"]) == tuple(key))]
+    return {"cases": len(recs),
+            "plan_first_ms": _mean_p95([r["plan_ms"][0] for r in recs]),
+            "plan_repeat_ms": _mean_p95([t for r in recs for t in r["plan_ms"][1:]]),
+            "select_mean_us": _mean_p95([r["select_us"]["mean"] for r in recs])}
 
 
 def main():

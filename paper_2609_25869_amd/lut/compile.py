@@ -347,6 +347,25 @@ def write_report(path: str, table, base, catalog, prof_recs, eval_recs, candidat
                   "A2 picks A1's plan in %.0f%% of the cases." % (sm["kernel"]["A0/A1"], sm["kernel"]["A0/A2"],
                                                                   sm["kernel"]["A2/A1"], 100 * sm["same_plan_as_A1"]),
                   ""]
+        rows = [("all keys", ablation.dispatch_summary(recs)),
+                ("64:64", ablation.dispatch_summary(recs, (64, 64)))]
+        if rows[0][1]["cases"]:
+            lines += ["## Dispatch overhead per request (the measurement of Table 7)", "",
+                      "`bsa_plan` is the whole request-path preprocessing: the mask state on the device, the one "
+                      "statistics copy and synchronisation, lookup and eligibility on the host, and the metadata "
+                      "launches of the selected plan (wall time, stream synchronised). The lookup and "
+                      "eligibility step alone is `bsa_select_plan` on the same statistics, called through the "
+                      "Python binding.", "",
+                      "| cases | n | `bsa_plan` first request mean / P95 (us) | `bsa_plan` repeats mean / P95 (us) "
+                      "| lookup + eligibility mean / P95 (us) |", "|---|---:|---:|---:|---:|"]
+            for name, d in rows:
+                if not d["cases"]:
+                    continue
+                pf, pr, se = d["plan_first_ms"], d["plan_repeat_ms"], d["select_mean_us"]
+                lines.append("| %s | %d | %.1f / %.1f | %.1f / %.1f | %.2f / %.2f |" % (
+                    name, d["cases"], 1e3 * pf["mean"], 1e3 * pf["p95"], 1e3 * pr["mean"], 1e3 * pr["p95"],
+                    se["mean"], se["p95"]))
+            lines.append("")
     with open(path, "w") as f:
         f.write("\n".join(lines))
 
