@@ -137,3 +137,18 @@ def test_request_ablation_summary():
     assert math.isclose(s["cold"]["A1/A2"], 40.0 / 1.6) and math.isclose(s["warm"]["A0/A2"], 2.0)
     assert math.isclose(s["amortized"]["A0/A1"], 2.0 / ((40 + 4.5) / 4))
     assert math.isclose(s["kernel"]["A0/A2"], 1.5) and s["same_plan_as_A1"] == 1.0
+
+
+def test_dispatch_summary_on_constructed_records():
+    from paper_2609_25869_amd.lut import ablation
+    recs = [{"key": [64, 64], "plan_ms": [0.30, 0.10, 0.12, 0.11], "select_us": {"mean": 1.0, "p95": 1.2}},
+            {"key": [128, 128], "plan_ms": [0.50, 0.20, 0.20, 0.20], "select_us": {"mean": 2.0, "p95": 2.5}},
+            {"key": [64, 64], "request_ms": {}}]  # a record without dispatch timings is left out
+    d = ablation.dispatch_summary(recs)
+    assert d["cases"] == 2
+    assert math.isclose(d["plan_first_ms"]["mean"], 0.40) and d["plan_first_ms"]["n"] == 2
+    assert d["plan_repeat_ms"]["n"] == 6 and math.isclose(d["plan_repeat_ms"]["mean"], (0.33 + 0.6) / 6)
+    assert math.isclose(d["select_mean_us"]["mean"], 1.5)
+    one = ablation.dispatch_summary(recs, (64, 64))
+    assert one["cases"] == 1 and math.isclose(one["plan_first_ms"]["p95"], 0.30)
+    assert ablation.dispatch_summary(recs, (32, 32))["plan_first_ms"] is None
