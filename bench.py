@@ -49,24 +49,27 @@ def effective_flops(mask, d):
     return 4 * d * total
 
 
-def gemm_probe(torch, n=8192, reps=10):
+def gemm_probe(torch, n=16384, reps=5, batches=3):
     """A practical bf16 MFMA ceiling on this machine: a large, contiguous
     n x n x n bf16 matrix product through the vendor GEMM library (fp32
-    accumulate), timed with HIP events after warm-up.  Returns TFLOP/s."""
+    accumulate), timed with HIP events after warm-up; the best of `batches`
+    batches of `reps` products.  Returns TFLOP/s."""
     a = torch.randn((n, n), device="cuda", dtype=torch.float32).to(torch.bfloat16)
     b = torch.randn((n, n), device="cuda", dtype=torch.float32).to(torch.bfloat16)
     c = torch.empty((n, n), device="cuda", dtype=torch.bfloat16)
-    for _ in range(3):
+    for _ in range(2):
         torch.matmul(a, b, out=c)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        torch.matmul(a, b, out=c)
-    e1.record()
-    e1.synchronize()
-    ms = e0.elapsed_time(e1) / reps
+    best = float("inf")
+    for _ in range(batches):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            torch.matmul(a, b, out=c)
+        e1.record()
+        e1.synchronize()
+        best = min(best, e0.elapsed_time(e1) / reps)
     del a, b, c
-    return 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+    return 2.0 * n ** 3 / (best * 1e-3) / 1e12
 
 
 def copy_probe(torch, mib):
@@ -320,7 +323,7 @@ def main():
     # outside the timed region: the practical MFMA ceiling of this machine
     probe = gemm_probe(torch)
     out["roofline"]["gemm_probe"] = {"tflops": probe, "frac": kernel_tflops / probe,
-                                     "what": "8192^3 bf16 torch.matmul (vendor GEMM), HIP events"}
+                                     "what": "16384^3 bf16 torch.matmul (vendor GEMM), best of 3 batches of 5, HIP events"}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle (about %.0f s)" % args.cpu_budget)
         out["cpu_baseline"] = cpu_baseline(q, k, v, mask, eff, args.cpu_budget)
