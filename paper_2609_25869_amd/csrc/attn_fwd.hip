@@ -466,7 +466,12 @@ void attn_fwd_kernel(AttnArgs a) {
   // of the same iteration.
   constexpr int kEAll = G * kE;           // score elements per lane, all groups
   constexpr int kGroupLoads = 2 * kLoadsPerWave;  // refill loads of one iteration
-  constexpr int kDmaEvery = kNU / kGroupLoads;
+  // Refill loads go out one every kDmaEvery units.  The T_Q = 64 kernels run
+  // one wave per SIMD, so no other workgroup covers a load still in flight
+  // at the barrier: they issue the whole refill at the start of the
+  // iteration (the slot it fills was released by the previous barrier).
+  // With two workgroups per CU, spreading the loads measured faster.
+  constexpr int kDmaEvery = NWAVES == 2 ? 1 : kNU / kGroupLoads;
   static_assert(kDmaEvery >= 1 && kDmaEvery * kGroupLoads <= kNU, "refill loads must fit the units");
   constexpr int kNS = kNU * G;            // MFMA slots of one iteration
   // elements whose exponential is formed by the end of slot ss
