@@ -153,6 +153,7 @@ def main():
     ap.add_argument("--workload", default="c2_window15")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gemm-probe", action="store_true", help="skip the vendor-GEMM ceiling probe")
     ap.add_argument("--force-plan", type=int, default=-1)
     ap.add_argument("--no-flush", action="store_true", help="skip the cache-evicting write before each step")
     ap.add_argument("--sparsify", action="store_true",
@@ -321,9 +322,11 @@ def main():
         out["sparsify_ms"] = {"mean": float(np.mean(sp)), "median": float(np.median(sp)), "topk": topk,
                               "in_request": True}
     # outside the timed region: the practical MFMA ceiling of this machine
-    probe = gemm_probe(torch)
-    out["roofline"]["gemm_probe"] = {"tflops": probe, "frac": kernel_tflops / probe,
-                                     "what": "16384^3 bf16 torch.matmul (vendor GEMM), best of 3 batches of 5, HIP events"}
+    if not args.no_gemm_probe:
+        probe = gemm_probe(torch)
+        out["roofline"]["gemm_probe"] = {"tflops": probe, "frac": kernel_tflops / probe,
+                                         "what": "16384^3 bf16 torch.matmul (vendor GEMM), best of 3 batches of 5, "
+                                                 "HIP events"}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle (about %.0f s)" % args.cpu_budget)
         out["cpu_baseline"] = cpu_baseline(q, k, v, mask, eff, args.cpu_budget)
