@@ -188,14 +188,16 @@ __device__ inline void block_sync() {
   asm volatile("" ::: "memory");
 }
 
-// Waves per SIMD the register budget is sized for: two for G = 1, one for
-// G = 2 (its accumulators and Q fragments need the whole register file).
-template <int G>
-constexpr int waves_per_simd() { return G == 1 ? 2 : 1; }
+// Waves per SIMD the register budget is sized for: two for G = 1 with four
+// or more waves per workgroup; one for G = 2 (its accumulators and Q
+// fragments need the whole register file) and for the 2-wave T_Q = 64
+// workgroups, whose 64 KB rings let only two workgroups share a CU.
+template <int NWAVES, int G>
+constexpr int waves_per_simd() { return (G == 1 && NWAVES > 2) ? 2 : 1; }
 
 template <int NWAVES, int G, int TKV, int STAGES>
-__global__ __launch_bounds__(64 * NWAVES) __attribute__((amdgpu_waves_per_eu(waves_per_simd<G>(),
-                                                                               waves_per_simd<G>())))
+__global__ __launch_bounds__(64 * NWAVES) __attribute__((amdgpu_waves_per_eu(waves_per_simd<NWAVES, G>(),
+                                                                               waves_per_simd<NWAVES, G>())))
 void attn_fwd_kernel(AttnArgs a) {
   using C = Cfg<NWAVES, G, TKV>;
   constexpr int kNKB = C::kNKB;
