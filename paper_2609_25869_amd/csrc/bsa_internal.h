@@ -52,6 +52,7 @@ struct MaskStateArgs {
   int32_t* col_idx;         // [nnz] (fill pass)
   SegStats* seg_stats;      // [nseg]
   unsigned long long* bh_nnz;  // [B*H]
+  int32_t wide;             // every mask row starts 4-byte aligned and nkb % 4 == 0
 };
 
 struct MapArgs {

@@ -25,6 +25,52 @@ __device__ inline int find_bh(const int64_t* row_base, int nbh, int64_t r) {
 
 __device__ inline uint64_t lanes_below(int lane) { return (lane == 0) ? 0ull : ((~0ull) >> (64 - lane)); }
 
+// Logical rows read as 32-bit words, for masks whose rows are 4-byte
+// aligned: a step covers 256 columns, lane l holding columns 4l .. 4l+3 (byte
+// j of its word is column 4l + j), and four ballots, one per byte position,
+// carry the step's activity.  Counts, runs and the compacted columns are the
+// same as those of the byte-wise walk.
+template <bool kFill>
+__device__ inline void mask_row_words(const MaskStateArgs& a, const uint8_t* row, int nkb, int64_t out_base, int lane,
+                                      int64_t r) {
+  const uint32_t* row32 = reinterpret_cast<const uint32_t*>(row);
+  const int nw = nkb >> 2;
+  int64_t nnz = 0, run = 0;
+  uint64_t carry = 0;  // activity of the column just before the current step
+  for (int w0 = 0; w0 < nw; w0 += 64) {
+    const int wi = w0 + lane;
+    // clamped addresses, so neither load sits behind a branch
+    const uint32_t x = row32[min(wi, nw - 1)];
+    const uint32_t xn = kFill ? 0u : row32[min(w0 + 64, nw - 1)];
+    const uint32_t word = wi < nw ? x : 0u;
+    uint64_t bb[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bb[j] = __ballot(((word >> (8 * j)) & 0xFFu) != 0);
+    if (kFill) {
+      const uint64_t below = lanes_below(lane);
+      int64_t pos = out_base + nnz + __popcll(bb[0] & below) + __popcll(bb[1] & below) + __popcll(bb[2] & below) +
+                    __popcll(bb[3] & below);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if ((bb[j] >> lane) & 1ull) a.col_idx[pos++] = 4 * wi + j;
+      }
+    } else {
+      // the first column after this step (for the run test of its last one)
+      const uint64_t next = (w0 + 64 < nw && (xn & 0xFFu) != 0) ? 1ull : 0ull;
+      const uint64_t left[4] = {(bb[3] << 1) | carry, bb[0], bb[1], bb[2]};
+      const uint64_t right[4] = {bb[1], bb[2], bb[3], (bb[0] >> 1) | (next << 63)};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) run += __popcll(bb[j] & (left[j] | right[j]));
+      carry = bb[3] >> 63;
+    }
+    nnz += __popcll(bb[0]) + __popcll(bb[1]) + __popcll(bb[2]) + __popcll(bb[3]);
+  }
+  if (!kFill && lane == 0) {
+    a.counts[r] = (int32_t)nnz;
+    a.runs[r] = (int32_t)run;
+  }
+}
+
 // Logical rows: count (with statistics) or fill the block-CSR columns.
 template <bool kFill>
 __global__ __launch_bounds__(256) void mask_rows_kernel(MaskStateArgs a) {
@@ -37,6 +83,10 @@ __global__ __launch_bounds__(256) void mask_rows_kernel(MaskStateArgs a) {
   const int64_t qb = r - a.row_base[bh];
   const uint8_t* row = a.mask + b * a.stride_b + hd.mask_off + qb * (int64_t)hd.nkb;
   const int64_t out_base = kFill ? a.row_ptr[r] : 0;
+  if (a.wide) {
+    mask_row_words<kFill>(a, row, hd.nkb, out_base, lane, r);
+    return;
+  }
   int64_t nnz = 0, run = 0;
   uint64_t carry = 0;  // activity of the column just before the current step
   for (int c0 = 0; c0 < hd.nkb; c0 += 64) {

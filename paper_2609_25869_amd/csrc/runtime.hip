@@ -292,6 +292,15 @@ bsa_status select_segment_plan(Segment& sg, const bsa_shapes& s, const bsa_plan_
 }  // namespace
 
 namespace {
+// Every logical mask row starts on a 4-byte boundary and spans whole words,
+// so the mask kernels may read rows as 32-bit words.
+bool mask_rows_word_aligned(const bsa_mask* mask, const std::vector<HeadDesc>& heads) {
+  if ((reinterpret_cast<uintptr_t>(mask->data) & 3) != 0 || (mask->stride_b & 3) != 0) return false;
+  for (const HeadDesc& hd : heads)
+    if ((hd.mask_off & 3) != 0 || (hd.nkb & 3) != 0) return false;
+  return true;
+}
+
 bsa_status read_device_i64(bsa_plan_t plan, const int64_t* src, int64_t* dst) {
   HIP_TRY(hipMemcpyAsync(dst, src, sizeof(int64_t), hipMemcpyDeviceToHost, plan->stream));
   HIP_TRY(hipStreamSynchronize(plan->stream));
@@ -540,6 +549,7 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
 
     // mu(M): row counts and statistics, then the block-CSR offsets
     MaskStateArgs ma{};
+    ma.wide = mask_rows_word_aligned(mask, p->heads) ? 1 : 0;
     ma.mask = mask->data;
     ma.stride_b = mask->stride_b;
     ma.heads = p->heads_dev;
@@ -602,6 +612,7 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
     ma.R = p->R;
     ma.row_ptr = p->row_ptr_dev;
     ma.col_idx = p->col_idx_dev;
+    ma.wide = mask_rows_word_aligned(mask, p->heads) ? 1 : 0;
     HIP_TRY(launch_mask_fill(ma, stream));
   }
   for (Segment& sg : p->segs) {
