@@ -69,6 +69,7 @@ struct MapArgs {
   const int64_t* tile_ptr;   // fill pass
   int32_t* tile_kv;
   uint64_t* member;          // may be null (no membership metadata)
+  int32_t wide;              // mask rows 4-byte aligned and nkb % 4 == 0 (see MaskStateArgs)
 };
 
 struct TaskArgs {

@@ -251,6 +251,52 @@ __global__ __launch_bounds__(256) void map_rows_kernel(MapArgs a) {
   }
   const int64_t out_base = kFill ? a.tile_ptr[rp] : 0;
   int64_t n = 0;
+  if (a.gq == 1 && a.gkv == 1 && a.wide) {
+    // Direct and Refined, word-aligned rows: lane l reads blocks 4l .. 4l+3
+    // of a step of 256 blocks; every active block kb contributes its tiles
+    // kb * rkv .. kb * rkv + rkv - 1 that exist (< npk), in ascending order.
+    const uint32_t* row32 = reinterpret_cast<const uint32_t*>(mh + (int64_t)qb0 * a.nkb);
+    const int nw = a.nkb >> 2;
+    for (int w0 = 0; w0 < nw; w0 += 64) {
+      const int wi = w0 + lane;
+      const uint32_t x = row32[min(wi, nw - 1)];
+      const uint32_t word = wi < nw ? x : 0u;
+      uint64_t bb[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bb[j] = __ballot(((word >> (8 * j)) & 0xFFu) != 0);
+      // Every block has rkv tiles except perhaps the row's last one (byte 3
+      // of word nw - 1), which has `deficit` fewer.  Tiles of the active
+      // blocks of the lanes below come first, then this lane's in order.
+      const uint64_t below = lanes_below(lane);
+      const int deficit = a.rkv - (a.npk - (a.nkb - 1) * a.rkv);
+      const int lw = nw - 1 - w0;  // lane holding the last block, if in this step
+      const bool last_active = lw >= 0 && lw < 64 && ((bb[3] >> lw) & 1ull);
+      int64_t before = (int64_t)a.rkv * (__popcll(bb[0] & below) + __popcll(bb[1] & below) +
+                                         __popcll(bb[2] & below) + __popcll(bb[3] & below));
+      if (last_active && lw < lane) before -= deficit;
+      const int64_t pos = out_base + n + before;
+      int64_t mine = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if ((bb[j] >> lane) & 1ull) {
+          const int kb = 4 * wi + j;
+          const int nt = min(a.rkv, a.npk - kb * a.rkv);
+          if (kFill) {
+            for (int s2 = 0; s2 < nt; ++s2) {
+              a.tile_kv[pos + mine + s2] = kb * a.rkv + s2;
+              if (a.member) a.member[pos + mine + s2] = 1ull;
+            }
+          }
+          mine += nt;
+        }
+      }
+      // this step's tile total
+      n += (int64_t)a.rkv * (__popcll(bb[0]) + __popcll(bb[1]) + __popcll(bb[2]) + __popcll(bb[3])) -
+           (last_active ? deficit : 0);
+    }
+    if (!kFill && lane == 0) a.counts[rp] = (int32_t)n;
+    return;
+  }
   if (a.gq == 1 && a.gkv == 1) {
     // Direct and Refined: one member per tile, the block (qb0, pk / rkv).
     // Every byte load of kMapBatch steps of 64 tiles is issued (from a

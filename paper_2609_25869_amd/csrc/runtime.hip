@@ -660,6 +660,7 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
       m.rkv = sg.rkv;
       m.Rp = sg.Rp;
       m.counts = sg.counts;
+      m.wide = mask_rows_word_aligned(mask, p->heads) ? 1 : 0;
       HIP_TRY(launch_map_count(m, stream));
       HIP_TRY(launch_scan_i32(sg.counts, sg.tile_ptr, sg.Rp, sg.scan_tmp, stream));
       m.tile_ptr = sg.tile_ptr;

@@ -28,6 +28,10 @@ CASES = [
     # sparse small blocks: tiles of 64-256 query rows span 2-8 query blocks,
     # so waves often have no active member in a tile (and skip it)
     ("g32_sparse", 1, 2, 1100, 1100, [(32, 32)] * 2, 0.08, 1),
+    # word-aligned mask rows (nKB % 4 == 0) whose last block has fewer
+    # refined tiles than the others (980 = 15 * 64 + 20, 950 = 7 * 128 + 54)
+    ("g64_tail", 1, 2, 980, 980, [(64, 64)] * 2, 0.3, 1),
+    ("g128_tail", 1, 2, 950, 950, [(128, 128)] * 2, 0.35, 1),
 ]
 
 
