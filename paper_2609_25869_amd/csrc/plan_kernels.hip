@@ -251,19 +251,36 @@ __global__ __launch_bounds__(256) void map_rows_kernel(MapArgs a) {
   }
   const int64_t out_base = kFill ? a.tile_ptr[rp] : 0;
   int64_t n = 0;
-  if (a.gq == 1 && a.gkv == 1 && a.wide) {
-    // Direct and Refined, word-aligned rows: lane l reads blocks 4l .. 4l+3
-    // of a step of 256 blocks; every active block kb contributes its tiles
-    // kb * rkv .. kb * rkv + rkv - 1 that exist (< npk), in ascending order.
-    const uint32_t* row32 = reinterpret_cast<const uint32_t*>(mh + (int64_t)qb0 * a.nkb);
+  if (a.gkv == 1 && a.wide) {
+    // One member block along KV per tile (Direct, Refined, Coarsened along Q,
+    // and Q-coarsened / KV-refined), word-aligned rows: lane l reads blocks
+    // 4l .. 4l+3 of a step of 256 blocks from each of the tile's nqm query
+    // rows; member bit a of block kb is row a's activity there.  Every block
+    // with a member active contributes its tiles kb * rkv .. kb * rkv + rkv - 1
+    // that exist (< npk), in ascending order, all with the block's bits.
+    const uint8_t* base = mh + (int64_t)qb0 * a.nkb;
     const int nw = a.nkb >> 2;
     for (int w0 = 0; w0 < nw; w0 += 64) {
       const int wi = w0 + lane;
-      const uint32_t x = row32[min(wi, nw - 1)];
-      const uint32_t word = wi < nw ? x : 0u;
+      const int wc = min(wi, nw - 1);
+      uint64_t mem[4] = {0ull, 0ull, 0ull, 0ull};
+      for (int a0 = 0; a0 < nqm; a0 += 4) {
+        // four rows' loads in flight at once (clamped rows, then masked)
+        uint32_t x[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          x[k] = reinterpret_cast<const uint32_t*>(base + (int64_t)min(a0 + k, nqm - 1) * a.nkb)[wc];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t word = (wi < nw && a0 + k < nqm) ? x[k] : 0u;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            mem[j] |= (((word >> (8 * j)) & 0xFFu) != 0 ? 1ull : 0ull) << (a0 + k);
+        }
+      }
       uint64_t bb[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) bb[j] = __ballot(((word >> (8 * j)) & 0xFFu) != 0);
+      for (int j = 0; j < 4; ++j) bb[j] = __ballot(mem[j] != 0);
       // Every block has rkv tiles except perhaps the row's last one (byte 3
       // of word nw - 1), which has `deficit` fewer.  Tiles of the active
       // blocks of the lanes below come first, then this lane's in order.
@@ -284,7 +301,7 @@ __global__ __launch_bounds__(256) void map_rows_kernel(MapArgs a) {
           if (kFill) {
             for (int s2 = 0; s2 < nt; ++s2) {
               a.tile_kv[pos + mine + s2] = kb * a.rkv + s2;
-              if (a.member) a.member[pos + mine + s2] = 1ull;
+              if (a.member) a.member[pos + mine + s2] = mem[j];
             }
           }
           mine += nt;
