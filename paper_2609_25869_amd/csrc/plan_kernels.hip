@@ -30,6 +30,8 @@ __device__ inline uint64_t lanes_below(int lane) { return (lane == 0) ? 0ull : (
 // j of its word is column 4l + j), and four ballots, one per byte position,
 // carry the step's activity.  Counts, runs and the compacted columns are the
 // same as those of the byte-wise walk.
+constexpr int kWordSteps = 4;  // word steps whose loads go out together
+
 template <bool kFill>
 __device__ inline void mask_row_words(const MaskStateArgs& a, const uint8_t* row, int nkb, int64_t out_base, int lane,
                                       int64_t r) {
@@ -37,33 +39,45 @@ __device__ inline void mask_row_words(const MaskStateArgs& a, const uint8_t* row
   const int nw = nkb >> 2;
   int64_t nnz = 0, run = 0;
   uint64_t carry = 0;  // activity of the column just before the current step
-  for (int w0 = 0; w0 < nw; w0 += 64) {
-    const int wi = w0 + lane;
-    // clamped addresses, so neither load sits behind a branch
-    const uint32_t x = row32[min(wi, nw - 1)];
-    const uint32_t xn = kFill ? 0u : row32[min(w0 + 64, nw - 1)];
-    const uint32_t word = wi < nw ? x : 0u;
-    uint64_t bb[4];
+  for (int w00 = 0; w00 < nw; w00 += 64 * kWordSteps) {
+    // the loads of kWordSteps steps (clamped addresses, none behind a branch)
+    uint32_t xs[kWordSteps];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bb[j] = __ballot(((word >> (8 * j)) & 0xFFu) != 0);
-    if (kFill) {
-      const uint64_t below = lanes_below(lane);
-      int64_t pos = out_base + nnz + __popcll(bb[0] & below) + __popcll(bb[1] & below) + __popcll(bb[2] & below) +
-                    __popcll(bb[3] & below);
+    for (int s = 0; s < kWordSteps; ++s) xs[s] = row32[min(w00 + 64 * s + lane, nw - 1)];
+    const uint32_t xn = kFill ? 0u : row32[min(w00 + 64 * kWordSteps, nw - 1)];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if ((bb[j] >> lane) & 1ull) a.col_idx[pos++] = 4 * wi + j;
+    for (int s = 0; s < kWordSteps; ++s) {
+      const int w0 = w00 + 64 * s;
+      if (w0 >= nw) break;
+      const int wi = w0 + lane;
+      const uint32_t word = wi < nw ? xs[s] : 0u;
+      uint64_t bb[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bb[j] = __ballot(((word >> (8 * j)) & 0xFFu) != 0);
+      if (kFill) {
+        const uint64_t below = lanes_below(lane);
+        int64_t pos = out_base + nnz + __popcll(bb[0] & below) + __popcll(bb[1] & below) +
+                      __popcll(bb[2] & below) + __popcll(bb[3] & below);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if ((bb[j] >> lane) & 1ull) a.col_idx[pos++] = 4 * wi + j;
+        }
+      } else {
+        // the first column after this step: byte 0 of the next step's lane 0
+        uint64_t next;
+        if (s + 1 < kWordSteps) {
+          next = (w0 + 64 < nw && (__shfl(xs[s + 1], 0, 64) & 0xFFu) != 0) ? 1ull : 0ull;
+        } else {
+          next = (w0 + 64 < nw && (xn & 0xFFu) != 0) ? 1ull : 0ull;
+        }
+        const uint64_t left[4] = {(bb[3] << 1) | carry, bb[0], bb[1], bb[2]};
+        const uint64_t right[4] = {bb[1], bb[2], bb[3], (bb[0] >> 1) | (next << 63)};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) run += __popcll(bb[j] & (left[j] | right[j]));
+        carry = bb[3] >> 63;
       }
-    } else {
-      // the first column after this step (for the run test of its last one)
-      const uint64_t next = (w0 + 64 < nw && (xn & 0xFFu) != 0) ? 1ull : 0ull;
-      const uint64_t left[4] = {(bb[3] << 1) | carry, bb[0], bb[1], bb[2]};
-      const uint64_t right[4] = {bb[1], bb[2], bb[3], (bb[0] >> 1) | (next << 63)};
-#pragma unroll
-      for (int j = 0; j < 4; ++j) run += __popcll(bb[j] & (left[j] | right[j]));
-      carry = bb[3] >> 63;
+      nnz += __popcll(bb[0]) + __popcll(bb[1]) + __popcll(bb[2]) + __popcll(bb[3]);
     }
-    nnz += __popcll(bb[0]) + __popcll(bb[1]) + __popcll(bb[2]) + __popcll(bb[3]);
   }
   if (!kFill && lane == 0) {
     a.counts[r] = (int32_t)nnz;
