@@ -42,6 +42,8 @@ CASES = [
     ("diag_only", 1, 2, 256, 256, 64, 64, 0, True),
     ("all_blocks", 1, 2, 256, 256, 64, 64, 100, True),
     ("many_cols", 1, 1, 300, 64 * 700 + 5, 64, 64, 37, True),
+    # the largest supported score row: 6144 KV blocks (the host rejects 6145)
+    ("max_kv_blocks", 1, 1, 128, 16 * 6144, 16, 16, 50, True),
 ]
 
 
