@@ -277,3 +277,66 @@ def test_plan_is_reusable_for_new_inputs():
         torch.cuda.synchronize()
         compare(bf16_to_f64(o2), O_ref, "reuse %d" % trial)
     p.destroy()
+
+
+def test_kv_rows_beyond_2_gib():
+    """One head's K/V rows reach past 2^31 bytes from the head's first token
+    (12 heads x 128 bf16 = 3 KB per token, 720,896 tokens): the kernel's
+    per-head 32-bit offsets must stay unsigned.  Every query block attends
+    to the same blocks on both sides of the 2 GiB mark plus one of its own;
+    the oracle evaluates the compact problem made of exactly those blocks
+    (Eq. 1 depends only on the active token pairs)."""
+    import torch
+    B, H, Nq, d, blk = 1, 12, 256, 128, 64
+    nkb = 11264
+    Nkv = nkb * blk
+    nqb = Nq // blk
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2024)
+    qd = torch.randn((B, Nq, H, d), generator=g, device="cuda").to(torch.bfloat16)
+    kd = torch.randn((B, Nkv, H, d), generator=g, device="cuda").to(torch.bfloat16)
+    vd = torch.randn((B, Nkv, H, d), generator=g, device="cuda").to(torch.bfloat16)
+    boundary = (1 << 31) // (H * d * 2) // blk          # first block past 2 GiB from token 0
+    common = [0, 5000, boundary - 1, boundary, boundary + 77, nkb - 1]
+    heads = []
+    for h in range(H):
+        m = np.zeros((nqb, nkb), dtype=np.uint8)
+        for qb in range(nqb):
+            m[qb, common] = 1
+            m[qb, boundary + 100 + 7 * qb + h] = 1
+        heads.append(m)
+    mask = BlockMask.from_heads([heads], [blk] * H, [blk] * H, Nq, Nkv)
+    md = torch.from_numpy(np.ascontiguousarray(mask.data)).cuda()
+    shapes = bsa.shapes_of(qd, kd, vd, qd)
+    assert all(bsa.plan_eligible(pid, blk, blk, shapes) for pid in (0, 4, 12, 16))
+
+    # the compact problem: the union of the active blocks, in order
+    union = sorted(set(common) | {boundary + 100 + 7 * qb + h for qb in range(nqb) for h in range(H)})
+    idx = torch.tensor([b * blk + t for b in union for t in range(blk)], device="cuda")
+    to_bits = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    q_bits = to_bits(qd)
+    k_bits, v_bits = to_bits(kd[:, idx]), to_bits(vd[:, idx])
+    pos = {b: i for i, b in enumerate(union)}
+    compact = []
+    for h in range(H):
+        mc = np.zeros((nqb, len(union)), dtype=np.uint8)
+        for qb in range(nqb):
+            for kb in np.nonzero(heads[h][qb])[0]:
+                mc[qb, pos[int(kb)]] = 1
+        compact.append(mc)
+    cmask = BlockMask.from_heads([compact], [blk] * H, [blk] * H, Nq, len(union) * blk)
+    O_ref, L_ref = oattn.masked_attention(q_bits, k_bits, v_bits, cmask)
+
+    for pid in (-1, 4, 0, 12, 16):
+        od = torch.empty_like(qd)
+        lsed = torch.empty((B, H, Nq), dtype=torch.float32, device="cuda")
+        p = bsa.plan(md, blk, blk, shapes, head_offset=list(mask.head_offset), stride_b=mask.stride_b,
+                     force_plan=pid)
+        bsa.forward(p, qd, kd, vd, od, lsed)
+        torch.cuda.synchronize()
+        log("  K/V past 2 GiB, plan %d" % p.info(0)["plan_id"])
+        compare(bf16_to_f64(od), O_ref, "kv>2GiB plan %d" % pid)
+        compare_lse(lsed.cpu().numpy().astype(np.float64), L_ref, "kv>2GiB plan %d" % pid)
+        p.destroy()
+    del qd, kd, vd
+    torch.cuda.empty_cache()
