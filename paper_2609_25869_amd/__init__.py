@@ -209,9 +209,11 @@ class Plan:
 
 def plan(mask, bq: Union[int, Sequence[int]], bkv: Union[int, Sequence[int]], shapes: Shapes,
          head_offset: Optional[Sequence[int]] = None, stride_b: int = 0, force_plan: int = -1,
-         select_mode: int = 0, lut: Optional[Lut] = None, stream=None) -> Plan:
+         select_mode: int = 0, lut: Optional[Lut] = None, stream=None, keep_row_order: bool = False) -> Plan:
     """Plan a request (bsa_plan).  `mask` is a CUDA uint8/bool tensor holding the
-    logical block masks; see include/bsa.h for its layout."""
+    logical block masks; see include/bsa.h for its layout.  keep_row_order
+    dispatches the tasks in row order instead of grouped by KV tile range
+    (same output)."""
     import torch
     if not (isinstance(mask, torch.Tensor) and mask.is_cuda and mask.dtype in (torch.uint8, torch.bool)):
         raise TypeError("mask must be a CUDA uint8 or bool tensor")
@@ -229,6 +231,7 @@ def plan(mask, bq: Union[int, Sequence[int]], bkv: Union[int, Sequence[int]], sh
     opts = PlanOpts()
     opts.force_plan, opts.select_mode = int(force_plan), int(select_mode)
     opts.lut = lut.handle if lut else None
+    opts.keep_row_order = 1 if keep_row_order else 0
     gq = (ctypes.c_int32 * len(bqs))(*bqs)
     gk = (ctypes.c_int32 * len(bkvs))(*bkvs)
     h = ctypes.c_void_p()

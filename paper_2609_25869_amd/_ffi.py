@@ -32,7 +32,7 @@ class Mask(ctypes.Structure):
 
 
 class PlanOpts(ctypes.Structure):
-    _fields_ = [("force_plan", c_i32), ("select_mode", c_i32), ("lut", c_vp)]
+    _fields_ = [("force_plan", c_i32), ("select_mode", c_i32), ("lut", c_vp), ("keep_row_order", c_i32)]
 
 
 class SegmentInfo(ctypes.Structure):

@@ -20,7 +20,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libbsa.so")
 
-SOURCES = ["runtime.hip", "plan_kernels.hip", "attn_fwd.hip", "sparsify.hip", "catalog.cpp"]
+SOURCES = ["runtime.hip", "plan_kernels.hip", "attn_fwd.hip", "sparsify.hip", "task_order.hip", "catalog.cpp"]
 ARCH = "gfx950"
 
 

@@ -237,8 +237,9 @@ void attn_fwd_kernel(AttnArgs a) {
   auto vslot = [&](int i) -> uint8_t* { return kslot(i) + C::kTileBytes; };
 
   const int64_t nt = a.ntasks_dev ? *a.ntasks_dev : a.ntasks;
-  const int64_t ti = task_of_slot(blockIdx.x, nt);
+  int64_t ti = task_of_slot(blockIdx.x, nt);
   if (ti < 0) return;
+  if (a.order) ti = ((const __attribute__((address_space(4))) int32_t*)a.order)[ti];
   const Task task = a.tasks[ti];
 
   const int tid = threadIdx.x;

@@ -84,10 +84,28 @@ struct TaskArgs {
   Task* tasks;
 };
 
+// Dispatch order of a segment's tasks (task_order.hip): a permutation of the
+// task indices, those of each (batch, head) sorted by (first KV tile, last KV
+// tile), stably.  Keys are (bh, first, last) in key_bits <= 64 bits.
+struct OrderArgs {
+  const Task* tasks;
+  const int64_t* ntasks_dev;  // device task count (may be null)
+  int64_t ntasks;             // exact count, or the bound when ntasks_dev is set
+  const int32_t* tile_kv;
+  int32_t tile_bits, key_bits;
+  uint64_t* keys_in;
+  uint64_t* keys_out;
+  int32_t* idx_in;
+  int32_t* order;             // out: [ntasks]; the first (device count) entries are the real tasks
+  void* temp;
+  size_t temp_bytes;
+};
+
 struct AttnArgs {
   const Task* tasks;
   int32_t ntasks;              // exact count, or an upper bound when ntasks_dev is set
   const int64_t* ntasks_dev;   // device count (may be null)
+  const int32_t* order;        // dispatch order of the tasks (may be null: as built)
   const int32_t* kv_tile;
   const uint64_t* member;      // null: every tile is fully active
   const uint16_t* q;
@@ -115,6 +133,11 @@ hipError_t launch_task_count(const TaskArgs& a, hipStream_t s);
 hipError_t launch_task_fill(const TaskArgs& a, hipStream_t s);
 hipError_t launch_attention(int tq, int tkv, const AttnArgs& a, hipStream_t s);
 bool attention_variant_exists(int tq, int tkv);
+// Key width for the dispatch order of tasks over nbh heads and ntiles KV tiles
+// per head (sets *tile_bits); the order is built only when it is <= 64.
+int task_order_key_bits(int64_t nbh, int64_t ntiles, int* tile_bits);
+hipError_t task_order_temp_bytes(int64_t n, int key_bits, size_t* bytes);
+hipError_t launch_task_order(const OrderArgs& a, hipStream_t s);
 hipError_t launch_splitk_merge(int tq, const AttnArgs& a, hipStream_t s);
 
 // Top-k sparsifier (sparsify.hip): block means of a [B, N, H, 128] bf16

@@ -173,6 +173,7 @@ struct Segment {
   Task* tasks = nullptr;
   int64_t* task_ptr = nullptr;  // split > 1: [Rp + 1], device task count at [Rp]
   int64_t tasks_bound = 0;
+  int32_t* order = nullptr;     // dispatch order of the tasks; null: row order
   float* ws = nullptr;
   int64_t ws_bytes = 0;
 };
@@ -629,6 +630,16 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
     const size_t o_mem = (direct || !coarse) ? 0 : take(sizeof(uint64_t) * (size_t)sg.tiles_bound);
     const size_t o_tasks = take(sizeof(Task) * (size_t)sg.tasks_bound);
     const size_t o_taskptr = e.split > 1 ? take(sizeof(int64_t) * (size_t)(sg.Rp + 1)) : 0;
+    // dispatch order: tasks of each head grouped by their KV tile range
+    int tile_bits = 0;
+    const int key_bits = task_order_key_bits((int64_t)B * H, sg.npk, &tile_bits);
+    const bool ordered = !opts.keep_row_order && key_bits <= 64 && sg.tasks_bound > 1;
+    size_t order_temp = 0;
+    if (ordered) HIP_TRY(task_order_temp_bytes(sg.tasks_bound, key_bits, &order_temp));
+    const size_t nb = ordered ? (size_t)sg.tasks_bound : 0;
+    const size_t o_kin = take(sizeof(uint64_t) * nb), o_kout = take(sizeof(uint64_t) * nb);
+    const size_t o_iin = take(sizeof(int32_t) * nb), o_order = take(sizeof(int32_t) * nb);
+    const size_t o_otemp = take(order_temp);
     void* buf = nullptr;
     if ((st = p->alloc(&buf, need)) != BSA_OK) return st;
     uint8_t* b8 = static_cast<uint8_t*>(buf);
@@ -691,6 +702,23 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
       sg.ws = static_cast<float*>(ws);
     }
     HIP_TRY(launch_task_fill(ta, stream));
+    if (ordered) {
+      OrderArgs oa{};
+      oa.tasks = sg.tasks;
+      oa.ntasks_dev = e.split > 1 ? sg.task_ptr + sg.Rp : nullptr;
+      oa.ntasks = sg.tasks_bound;
+      oa.tile_kv = sg.tile_kv;
+      oa.tile_bits = tile_bits;
+      oa.key_bits = key_bits;
+      oa.keys_in = reinterpret_cast<uint64_t*>(b8 + o_kin);
+      oa.keys_out = reinterpret_cast<uint64_t*>(b8 + o_kout);
+      oa.idx_in = reinterpret_cast<int32_t*>(b8 + o_iin);
+      oa.order = reinterpret_cast<int32_t*>(b8 + o_order);
+      oa.temp = b8 + o_otemp;
+      oa.temp_bytes = order_temp;
+      HIP_TRY(launch_task_order(oa, stream));
+      sg.order = oa.order;
+    }
   }
   HIP_TRY(hipEventRecord(p->ready, stream));
   *out = p.release();
@@ -714,6 +742,7 @@ bsa_status bsa_forward(bsa_plan_t plan, const void* q, const void* k, const void
     a.tasks = sg.tasks;
     a.ntasks = (int32_t)sg.tasks_bound;
     a.ntasks_dev = e.split > 1 ? sg.task_ptr + sg.Rp : nullptr;
+    a.order = sg.order;
     a.kv_tile = sg.tile_kv;
     a.member = sg.member;
     a.q = static_cast<const uint16_t*>(q);

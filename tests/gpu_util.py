@@ -32,20 +32,23 @@ def mask_to_dev(mask):
 
 
 def run_plan(bsa, mask, q, k, v, force_plan: int = -1, lse: bool = True, select_mode: int = 0,
-             geometry_per_head: Optional[bool] = None):
-    """Plan and run on device; returns (plan, O tensor, LSE tensor or None, device inputs)."""
+             geometry_per_head: Optional[bool] = None, keep_row_order: bool = False):
+    """Plan and run on device; returns (plan, O tensor, LSE tensor or None, device inputs).
+
+    O and LSE start as NaN, so a row that no task writes cannot pass for a
+    correct one left in reused memory by an earlier run."""
     import torch
     qd, kd, vd = to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v)
-    od = torch.empty_like(qd)
+    od = torch.full_like(qd, float("nan"))
     B, Nq, H, d = q.shape
-    lsed = torch.empty((B, H, Nq), dtype=torch.float32, device="cuda") if lse else None
+    lsed = torch.full((B, H, Nq), float("nan"), dtype=torch.float32, device="cuda") if lse else None
     md = mask_to_dev(mask)
     shapes = bsa.shapes_of(qd, kd, vd, od)
     per_head = (not mask.uniform_geometry) if geometry_per_head is None else geometry_per_head
     bq = list(mask.bq) if per_head else int(mask.bq[0])
     bkv = list(mask.bkv) if per_head else int(mask.bkv[0])
     p = bsa.plan(md, bq, bkv, shapes, head_offset=list(mask.head_offset), stride_b=mask.stride_b,
-                 force_plan=force_plan, select_mode=select_mode)
+                 force_plan=force_plan, select_mode=select_mode, keep_row_order=keep_row_order)
     bsa.forward(p, qd, kd, vd, od, lsed)
     torch.cuda.synchronize()
     return p, od, lsed, (qd, kd, vd, md)
