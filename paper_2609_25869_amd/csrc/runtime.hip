@@ -52,6 +52,9 @@ int ilog2_exact(int64_t x) {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Task count above which the planner sorts a segment's tasks into KV order.
+constexpr int64_t kOrderMinTasks = 512;
+
 // ---------------------------------------------------------------------------
 // Pinned staging for the per-request host<->device copies.  One buffer per
 // process, reused; the lock is held from the upload until the request's one
@@ -630,10 +633,12 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
     const size_t o_mem = (direct || !coarse) ? 0 : take(sizeof(uint64_t) * (size_t)sg.tiles_bound);
     const size_t o_tasks = take(sizeof(Task) * (size_t)sg.tasks_bound);
     const size_t o_taskptr = e.split > 1 ? take(sizeof(int64_t) * (size_t)(sg.Rp + 1)) : 0;
-    // dispatch order: tasks of each head grouped by their KV tile range
+    // dispatch order: tasks of each head grouped by their KV tile range.  Up
+    // to 512 tasks (two workgroups on each of 256 CUs) run all at once, so
+    // their order does not change what shares an L2.
     int tile_bits = 0;
     const int key_bits = task_order_key_bits((int64_t)B * H, sg.npk, &tile_bits);
-    const bool ordered = !opts.keep_row_order && key_bits <= 64 && sg.tasks_bound > 1;
+    const bool ordered = !opts.keep_row_order && key_bits <= 64 && sg.tasks_bound > kOrderMinTasks;
     size_t order_temp = 0;
     if (ordered) HIP_TRY(task_order_temp_bytes(sg.tasks_bound, key_bits, &order_temp));
     const size_t nb = ordered ? (size_t)sg.tasks_bound : 0;

@@ -343,13 +343,14 @@ def test_kv_rows_beyond_2_gib():
 
 
 def test_dispatch_order_does_not_change_the_output():
-    """Tasks dispatched grouped by KV tile range (the default) and in row order
-    give the same bits, and every row is written (outputs start as NaN).  A
-    3-D window over a (4, 3, 5) grid of 64-token blocks: query blocks with
-    equal KV lists sit a grid stride apart in row order."""
+    """Tasks dispatched grouped by KV tile range (the default above 512 tasks)
+    and in row order give the same bits, every row is written (outputs start
+    as NaN), and both match the oracle.  A 3-D window over an (8, 4, 4) grid
+    of 64-token blocks, 12 heads: query blocks with equal KV lists sit a grid
+    stride apart in row order."""
     import torch
     from workloads.gen import window_mask
-    grid, half, bs, H = (4, 3, 5), (1, 2, 1), 64, 2
+    grid, half, bs, H = (8, 4, 4), (1, 1, 1), 64, 12
     blocks = window_mask(grid, half).astype(np.uint8)
     N = blocks.shape[0] * bs
     rng = np.random.default_rng(91)
@@ -357,13 +358,17 @@ def test_dispatch_order_does_not_change_the_output():
     mask = BlockMask.from_heads([[blocks] * H], [bs] * H, [bs] * H, N, N)
     O_ref, L_ref = oattn.masked_attention(q, k, v, mask)
     ids = _eligible_plans(mask)
-    assert any(e["split"] > 1 for e in bsa.catalog() if e["id"] in ids)
+    split_ids = [e["id"] for e in bsa.catalog() if e["id"] in ids and e["split"] > 1]
+    assert split_ids
+    ordered = 0
     for pid in [-1] + ids:
         log("dispatch order, plan %d" % pid)
         p1, o1, l1, _ = run_plan(bsa, mask, q, k, v, force_plan=pid)
         p2, o2, l2, _ = run_plan(bsa, mask, q, k, v, force_plan=pid, keep_row_order=True)
+        ordered += p1.info()["n_tasks"] > 512
         assert torch.equal(o1, o2) and torch.equal(l1, l2), "plan %d: the dispatch order changed the output" % pid
         compare(bf16_to_f64(o1), O_ref, "dispatch order plan %d" % pid)
         compare_lse(l1.cpu().numpy().astype(np.float64), L_ref, "dispatch order plan %d" % pid)
         p1.destroy()
         p2.destroy()
+    assert ordered >= len(ids) // 2, "too few plans with more than 512 tasks"
