@@ -97,6 +97,7 @@ struct OrderArgs {
   uint64_t* keys_out;
   int32_t* idx_in;
   int32_t* order;             // out: [ntasks]; the first (device count) entries are the real tasks
+  Task* tasks_out;            // out (may be null): tasks[order[i]] at i; only without a device count
   void* temp;
   size_t temp_bytes;
 };

@@ -176,7 +176,8 @@ struct Segment {
   Task* tasks = nullptr;
   int64_t* task_ptr = nullptr;  // split > 1: [Rp + 1], device task count at [Rp]
   int64_t tasks_bound = 0;
-  int32_t* order = nullptr;     // dispatch order of the tasks; null: row order
+  int32_t* order = nullptr;     // dispatch order of the tasks (Split-K plans); null: as stored
+  Task* tasks_run = nullptr;    // the tasks in dispatch order (plans without Split-K); null: row order
   float* ws = nullptr;
   int64_t ws_bytes = 0;
 };
@@ -645,6 +646,7 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
     const size_t o_kin = take(sizeof(uint64_t) * nb), o_kout = take(sizeof(uint64_t) * nb);
     const size_t o_iin = take(sizeof(int32_t) * nb), o_order = take(sizeof(int32_t) * nb);
     const size_t o_otemp = take(order_temp);
+    const size_t o_trun = take(e.split == 1 ? sizeof(Task) * nb : 0);
     void* buf = nullptr;
     if ((st = p->alloc(&buf, need)) != BSA_OK) return st;
     uint8_t* b8 = static_cast<uint8_t*>(buf);
@@ -721,8 +723,12 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
       oa.order = reinterpret_cast<int32_t*>(b8 + o_order);
       oa.temp = b8 + o_otemp;
       oa.temp_bytes = order_temp;
+      oa.tasks_out = e.split == 1 ? reinterpret_cast<Task*>(b8 + o_trun) : nullptr;
       HIP_TRY(launch_task_order(oa, stream));
-      sg.order = oa.order;
+      // without Split-K the kernel reads the reordered copy directly; the
+      // row-order list stays for the plan export
+      sg.tasks_run = oa.tasks_out;
+      sg.order = e.split == 1 ? nullptr : oa.order;
     }
   }
   HIP_TRY(hipEventRecord(p->ready, stream));
@@ -744,7 +750,7 @@ bsa_status bsa_forward(bsa_plan_t plan, const void* q, const void* k, const void
   for (const Segment& sg : plan->segs) {
     const CatalogEntry& e = sg.plan;
     AttnArgs a{};
-    a.tasks = sg.tasks;
+    a.tasks = sg.tasks_run ? sg.tasks_run : sg.tasks;
     a.ntasks = (int32_t)sg.tasks_bound;
     a.ntasks_dev = e.split > 1 ? sg.task_ptr + sg.Rp : nullptr;
     a.order = sg.order;

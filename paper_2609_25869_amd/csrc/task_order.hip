@@ -41,6 +41,15 @@ __global__ __launch_bounds__(256) void task_key_kernel(OrderArgs a) {
   a.idx_in[t] = (int32_t)t;
 }
 
+// The tasks themselves in dispatch order, so the kernel reads its task with
+// no indirection (tasks without Split-K partners only: the merge finds the
+// partial states of a row's pieces next to each other in row order).
+__global__ __launch_bounds__(256) void task_gather_kernel(OrderArgs a) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= a.ntasks) return;
+  a.tasks_out[t] = a.tasks[a.order[t]];
+}
+
 }  // namespace
 
 int task_order_key_bits(int64_t nbh, int64_t ntiles, int* tile_bits) {
@@ -67,8 +76,11 @@ hipError_t launch_task_order(const OrderArgs& a, hipStream_t s) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   size_t bytes = a.temp_bytes;
-  return hipcub::DeviceRadixSort::SortPairs(a.temp, bytes, a.keys_in, a.keys_out, a.idx_in, a.order,
-                                            (int)a.ntasks, 0, a.key_bits, s);
+  e = hipcub::DeviceRadixSort::SortPairs(a.temp, bytes, a.keys_in, a.keys_out, a.idx_in, a.order, (int)a.ntasks, 0,
+                                         a.key_bits, s);
+  if (e != hipSuccess || !a.tasks_out) return e;
+  hipLaunchKernelGGL(task_gather_kernel, dim3((unsigned)((a.ntasks + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 }  // namespace bsa
