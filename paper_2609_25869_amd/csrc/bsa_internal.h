@@ -85,18 +85,23 @@ struct TaskArgs {
 };
 
 // Dispatch order of a segment's tasks (task_order.hip): a permutation of the
-// task indices, those of each (batch, head) sorted by (first KV tile, last KV
-// tile), stably.  Keys are (bh, first, last) in key_bits <= 64 bits.
+// task indices, row order with every task moved up to the first task that
+// has the same KV tile list (and member bits).  Work arrays are [ntasks].
 struct OrderArgs {
   const Task* tasks;
   const int64_t* ntasks_dev;  // device task count (may be null)
   int64_t ntasks;             // exact count, or the bound when ntasks_dev is set
   const int32_t* tile_kv;
-  int32_t tile_bits, key_bits;
-  uint64_t* keys_in;
+  const uint64_t* member;     // may be null
+  uint64_t* keys_in;          // list hashes
   uint64_t* keys_out;
   int32_t* idx_in;
-  int32_t* order;             // out: [ntasks]; the first (device count) entries are the real tasks
+  int32_t* idx_sorted;
+  int32_t* head_pos;
+  int32_t* head_run;
+  uint32_t* rep;              // representative task of each task
+  uint32_t* rep_sorted;
+  int32_t* order;             // out; the first (device count) entries are the real tasks
   Task* tasks_out;            // out (may be null): tasks[order[i]] at i; only without a device count
   void* temp;
   size_t temp_bytes;
@@ -134,10 +139,7 @@ hipError_t launch_task_count(const TaskArgs& a, hipStream_t s);
 hipError_t launch_task_fill(const TaskArgs& a, hipStream_t s);
 hipError_t launch_attention(int tq, int tkv, const AttnArgs& a, hipStream_t s);
 bool attention_variant_exists(int tq, int tkv);
-// Key width for the dispatch order of tasks over nbh heads and ntiles KV tiles
-// per head (sets *tile_bits); the order is built only when it is <= 64.
-int task_order_key_bits(int64_t nbh, int64_t ntiles, int* tile_bits);
-hipError_t task_order_temp_bytes(int64_t n, int key_bits, size_t* bytes);
+hipError_t task_order_temp_bytes(int64_t n, size_t* bytes);
 hipError_t launch_task_order(const OrderArgs& a, hipStream_t s);
 hipError_t launch_splitk_merge(int tq, const AttnArgs& a, hipStream_t s);
 

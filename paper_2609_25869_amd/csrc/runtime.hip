@@ -634,17 +634,18 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
     const size_t o_mem = (direct || !coarse) ? 0 : take(sizeof(uint64_t) * (size_t)sg.tiles_bound);
     const size_t o_tasks = take(sizeof(Task) * (size_t)sg.tasks_bound);
     const size_t o_taskptr = e.split > 1 ? take(sizeof(int64_t) * (size_t)(sg.Rp + 1)) : 0;
-    // dispatch order: tasks of each head grouped by their KV tile range.  Up
-    // to 512 tasks (two workgroups on each of 256 CUs) run all at once, so
-    // their order does not change what shares an L2.
-    int tile_bits = 0;
-    const int key_bits = task_order_key_bits((int64_t)B * H, sg.npk, &tile_bits);
-    const bool ordered = !opts.keep_row_order && key_bits <= 64 && sg.tasks_bound > kOrderMinTasks;
+    // dispatch order: tasks with equal KV lists side by side.  Up to 512
+    // tasks (two workgroups on each of 256 CUs) run all at once, so their
+    // order does not change what shares an L2.
+    const bool ordered = !opts.keep_row_order && sg.tasks_bound > kOrderMinTasks;
     size_t order_temp = 0;
-    if (ordered) HIP_TRY(task_order_temp_bytes(sg.tasks_bound, key_bits, &order_temp));
+    if (ordered) HIP_TRY(task_order_temp_bytes(sg.tasks_bound, &order_temp));
     const size_t nb = ordered ? (size_t)sg.tasks_bound : 0;
     const size_t o_kin = take(sizeof(uint64_t) * nb), o_kout = take(sizeof(uint64_t) * nb);
-    const size_t o_iin = take(sizeof(int32_t) * nb), o_order = take(sizeof(int32_t) * nb);
+    const size_t o_iin = take(sizeof(int32_t) * nb), o_isort = take(sizeof(int32_t) * nb);
+    const size_t o_hpos = take(sizeof(int32_t) * nb), o_hrun = take(sizeof(int32_t) * nb);
+    const size_t o_rep = take(sizeof(uint32_t) * nb), o_rsort = take(sizeof(uint32_t) * nb);
+    const size_t o_order = take(sizeof(int32_t) * nb);
     const size_t o_otemp = take(order_temp);
     const size_t o_trun = take(e.split == 1 ? sizeof(Task) * nb : 0);
     void* buf = nullptr;
@@ -715,11 +716,15 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
       oa.ntasks_dev = e.split > 1 ? sg.task_ptr + sg.Rp : nullptr;
       oa.ntasks = sg.tasks_bound;
       oa.tile_kv = sg.tile_kv;
-      oa.tile_bits = tile_bits;
-      oa.key_bits = key_bits;
+      oa.member = sg.member;
       oa.keys_in = reinterpret_cast<uint64_t*>(b8 + o_kin);
       oa.keys_out = reinterpret_cast<uint64_t*>(b8 + o_kout);
       oa.idx_in = reinterpret_cast<int32_t*>(b8 + o_iin);
+      oa.idx_sorted = reinterpret_cast<int32_t*>(b8 + o_isort);
+      oa.head_pos = reinterpret_cast<int32_t*>(b8 + o_hpos);
+      oa.head_run = reinterpret_cast<int32_t*>(b8 + o_hrun);
+      oa.rep = reinterpret_cast<uint32_t*>(b8 + o_rep);
+      oa.rep_sorted = reinterpret_cast<uint32_t*>(b8 + o_rsort);
       oa.order = reinterpret_cast<int32_t*>(b8 + o_order);
       oa.temp = b8 + o_otemp;
       oa.temp_bytes = order_temp;

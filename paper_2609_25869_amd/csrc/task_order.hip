@@ -4,14 +4,16 @@
 // order, and an XCD holds a few dozen tasks at once that all stream K/V
 // tiles through its own L2.  Two tasks share L2 lines only if they read the
 // same tile at nearly the same time, which in practice means their tile lists
-// are equal and they start together.  Tasks built in row order rarely are:
-// under a multi-dimensional window, query blocks with equal KV lists sit a
-// grid stride apart, and tasks with shorter lists drift ahead of the others.
-// Sorting the tasks of each (batch, head) by their first and then their last
-// KV tile puts equal lists next to each other, so they are dispatched
-// together, finish together, and their successors start together.  The sort
-// is stable: tasks with equal keys keep their row order.  Every task still
-// computes exactly what it computed before, so results do not change.
+// are equal and they start together.  In row order that happens only by
+// chance: under a multi-dimensional window, query blocks with equal KV lists
+// sit a grid stride apart, and tasks with shorter lists drift ahead of the
+// others.  The order used here is row order, except that every task moves up
+// to the first task (in row order) with the same KV tile list: equal lists
+// are dispatched together, finish together, and hand their slots to the next
+// group together, while rows whose lists are unique keep the row order, in
+// which neighbouring rows usually read overlapping lists.  Every task still
+// computes exactly what it computed before, so results do not change; a hash
+// collision can only cost locality.
 #include <hipcub/hipcub.hpp>
 
 #include "bsa_internal.h"
@@ -20,25 +22,64 @@ namespace bsa {
 
 namespace {
 
-// Key of task t: (bh, first tile, last tile) packed into key_bits bits.
-// Entries past the device task count get the largest key, so the stable
-// sort leaves the real tasks in front.
-__global__ __launch_bounds__(256) void task_key_kernel(OrderArgs a) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// SplitMix64 finaliser (Steele, Lea and Flood, "Fast splittable
+// pseudorandom number generators", OOPSLA 2014).
+__device__ inline uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+constexpr int kWavesPerBlock = 4;
+
+// Key of task t: a hash of (bh, tile count, tile list, member bits), one
+// wave per task.  Entries past the device task count get the key ~0; the
+// representative pass keeps them behind every real task whatever their key.
+__global__ __launch_bounds__(64 * kWavesPerBlock) void task_hash_kernel(OrderArgs a) {
+  const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   if (t >= a.ntasks) return;
   const int64_t nt = a.ntasks_dev ? *a.ntasks_dev : a.ntasks;
-  uint64_t key = a.key_bits >= 64 ? ~0ull : ((1ull << a.key_bits) - 1);
+  uint64_t key = ~0ull;
   if (t < nt) {
     const Task tk = a.tasks[t];
-    uint64_t first = 0, last = 0;
-    if (tk.tile_end > tk.tile_begin) {
-      first = (uint32_t)a.tile_kv[tk.tile_begin];
-      last = (uint32_t)a.tile_kv[tk.tile_end - 1];
+    const int64_t n = (int64_t)tk.tile_end - tk.tile_begin;
+    uint64_t h = 0;
+    for (int64_t i = lane; i < n; i += 64) {
+      const uint64_t kv = (uint32_t)a.tile_kv[tk.tile_begin + i];
+      const uint64_t mem = a.member ? a.member[tk.tile_begin + i] : 0ull;
+      h += mix64(kv | ((uint64_t)i << 32)) ^ mix64(mem + 0x9e3779b97f4a7c15ull * (uint64_t)(i + 1));
     }
-    key = ((uint64_t)(uint32_t)tk.bh << (2 * a.tile_bits)) | (first << a.tile_bits) | last;
+    for (int off = 32; off > 0; off >>= 1) h += __shfl_xor(h, off);
+    key = mix64(h ^ mix64(((uint64_t)(uint32_t)tk.bh << 32) | (uint64_t)(uint32_t)n));
   }
-  a.keys_in[t] = key;
-  a.idx_in[t] = (int32_t)t;
+  if (lane == 0) {
+    a.keys_in[t] = key;
+    a.idx_in[t] = (int32_t)t;
+  }
+}
+
+// Position p of the hash-sorted list: 1 + p where a run of equal keys starts, else 0.
+__global__ __launch_bounds__(256) void run_head_kernel(OrderArgs a) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= a.ntasks) return;
+  a.head_pos[p] = (p == 0 || a.keys_out[p] != a.keys_out[p - 1]) ? (int32_t)(p + 1) : 0;
+}
+
+// Representative of each task: the first task (lowest index) of its run of
+// equal keys; tasks past the device count represent themselves.
+__global__ __launch_bounds__(256) void representative_kernel(OrderArgs a) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= a.ntasks) return;
+  const int64_t nt = a.ntasks_dev ? *a.ntasks_dev : a.ntasks;
+  const int32_t t = a.idx_sorted[p];
+  const int32_t head = a.head_run[p] - 1;  // inclusive max-scan of run_head_kernel's output
+  a.rep[t] = t >= nt ? (uint32_t)t : (uint32_t)a.idx_sorted[head];
+}
+
+__global__ __launch_bounds__(256) void iota_kernel(int32_t* v, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) v[i] = (int32_t)i;
 }
 
 // The tasks themselves in dispatch order, so the kernel reads its task with
@@ -50,36 +91,68 @@ __global__ __launch_bounds__(256) void task_gather_kernel(OrderArgs a) {
   a.tasks_out[t] = a.tasks[a.order[t]];
 }
 
-}  // namespace
+struct MaxOp {
+  __device__ int32_t operator()(int32_t x, int32_t y) const { return x > y ? x : y; }
+};
 
-int task_order_key_bits(int64_t nbh, int64_t ntiles, int* tile_bits) {
-  auto bits_for = [](int64_t n) {  // bits of the largest index n - 1, at least 1
-    int b = 1;
-    while (b < 63 && (int64_t(1) << b) < n) ++b;
-    return b;
-  };
-  *tile_bits = bits_for(ntiles);
-  return bits_for(nbh) + 2 * *tile_bits;
+int rep_bits(int64_t n) {  // bits of the largest task index n - 1, at least 1
+  int b = 1;
+  while (b < 31 && (int64_t(1) << b) < n) ++b;
+  return b;
 }
 
-hipError_t task_order_temp_bytes(int64_t n, int key_bits, size_t* bytes) {
+unsigned grid(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+hipError_t task_order_temp_bytes(int64_t n, size_t* bytes) {
   *bytes = 0;
   if (n <= 1) return hipSuccess;
-  return hipcub::DeviceRadixSort::SortPairs(nullptr, *bytes, static_cast<const uint64_t*>(nullptr),
-                                            static_cast<uint64_t*>(nullptr), static_cast<const int32_t*>(nullptr),
-                                            static_cast<int32_t*>(nullptr), (int)n, 0, key_bits, (hipStream_t)0);
+  size_t b1 = 0, b2 = 0, b3 = 0;
+  hipError_t e = hipcub::DeviceRadixSort::SortPairs(nullptr, b1, static_cast<const uint64_t*>(nullptr),
+                                                    static_cast<uint64_t*>(nullptr),
+                                                    static_cast<const int32_t*>(nullptr),
+                                                    static_cast<int32_t*>(nullptr), (int)n, 0, 64, (hipStream_t)0);
+  if (e != hipSuccess) return e;
+  e = hipcub::DeviceScan::InclusiveScan(nullptr, b2, static_cast<const int32_t*>(nullptr),
+                                        static_cast<int32_t*>(nullptr), MaxOp(), (int)n, (hipStream_t)0);
+  if (e != hipSuccess) return e;
+  e = hipcub::DeviceRadixSort::SortPairs(nullptr, b3, static_cast<const uint32_t*>(nullptr),
+                                         static_cast<uint32_t*>(nullptr), static_cast<const int32_t*>(nullptr),
+                                         static_cast<int32_t*>(nullptr), (int)n, 0, rep_bits(n), (hipStream_t)0);
+  *bytes = std::max(b1, std::max(b2, b3));
+  return e;
 }
 
 hipError_t launch_task_order(const OrderArgs& a, hipStream_t s) {
-  if (a.ntasks <= 1) return hipSuccess;
-  hipLaunchKernelGGL(task_key_kernel, dim3((unsigned)((a.ntasks + 255) / 256)), dim3(256), 0, s, a);
+  const int64_t n = a.ntasks;
+  if (n <= 1) return hipSuccess;
+  size_t bytes = a.temp_bytes;
+  // 1. hash every task's list; sort (hash, index) so equal lists form runs,
+  //    lowest index first (the sort is stable)
+  hipLaunchKernelGGL(task_hash_kernel, dim3(grid(n, kWavesPerBlock)), dim3(64 * kWavesPerBlock), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  size_t bytes = a.temp_bytes;
-  e = hipcub::DeviceRadixSort::SortPairs(a.temp, bytes, a.keys_in, a.keys_out, a.idx_in, a.order, (int)a.ntasks, 0,
-                                         a.key_bits, s);
+  e = hipcub::DeviceRadixSort::SortPairs(a.temp, bytes, a.keys_in, a.keys_out, a.idx_in, a.idx_sorted, (int)n, 0, 64,
+                                         s);
+  if (e != hipSuccess) return e;
+  // 2. each task's representative: the first index of its run
+  hipLaunchKernelGGL(run_head_kernel, dim3(grid(n, 256)), dim3(256), 0, s, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  bytes = a.temp_bytes;
+  e = hipcub::DeviceScan::InclusiveScan(a.temp, bytes, a.head_pos, a.head_run, MaxOp(), (int)n, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(representative_kernel, dim3(grid(n, 256)), dim3(256), 0, s, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  // 3. order by (representative, index): row order with equal lists pulled
+  //    up to their first occurrence
+  hipLaunchKernelGGL(iota_kernel, dim3(grid(n, 256)), dim3(256), 0, s, a.idx_in, n);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  bytes = a.temp_bytes;
+  e = hipcub::DeviceRadixSort::SortPairs(a.temp, bytes, a.rep, a.rep_sorted, a.idx_in, a.order, (int)n, 0, rep_bits(n),
+                                         s);
   if (e != hipSuccess || !a.tasks_out) return e;
-  hipLaunchKernelGGL(task_gather_kernel, dim3((unsigned)((a.ntasks + 255) / 256)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(task_gather_kernel, dim3(grid(n, 256)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

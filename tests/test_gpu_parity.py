@@ -343,14 +343,15 @@ def test_kv_rows_beyond_2_gib():
 
 
 def test_dispatch_order_does_not_change_the_output():
-    """Tasks dispatched grouped by KV tile range (the default above 512 tasks)
-    and in row order give the same bits, every row is written (outputs start
-    as NaN), and both match the oracle.  A 3-D window over an (8, 4, 4) grid
-    of 64-token blocks, 12 heads: query blocks with equal KV lists sit a grid
-    stride apart in row order."""
+    """Tasks dispatched with equal KV lists side by side (the default above 512
+    tasks) and in row order give the same bits, every row is written (outputs
+    start as NaN), and both match the oracle.  A 3-D window over an (8, 4, 4)
+    grid of 64-token blocks whose middle half-width covers the whole grid, so
+    the four query blocks of a (t, w) pair have equal KV lists and sit a grid
+    stride apart in row order; 10 heads."""
     import torch
     from workloads.gen import window_mask
-    grid, half, bs, H = (8, 4, 4), (1, 1, 1), 64, 12
+    grid, half, bs, H = (8, 4, 4), (1, 3, 1), 64, 10
     blocks = window_mask(grid, half).astype(np.uint8)
     N = blocks.shape[0] * bs
     rng = np.random.default_rng(91)
