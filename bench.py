@@ -27,6 +27,7 @@ PEAK_HBM_GBS = 8000.0
 
 FLUSH_BYTES = 512 << 20
 KERNEL_SRC = os.path.join(HERE, "paper_2609_25869_amd", "csrc", "attn_fwd.hip")
+ORDER_SRC = os.path.join(HERE, "paper_2609_25869_amd", "csrc", "task_order.hip")  # dispatch order: sets L2 reuse
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "attn_fwd_c2_window15_traffic.md")
 
 
@@ -87,7 +88,7 @@ def measured_traffic(workload, plan_ids):
     """HBM bytes per launch of the attention kernel from the committed counter summary.
 
     Reported only when that summary was taken on this workload and plan with
-    the current kernel source; otherwise None.
+    the current kernel and dispatch-order sources; otherwise None.
     """
     import hashlib
     if not os.path.exists(TRAFFIC_FILE):
@@ -98,7 +99,9 @@ def measured_traffic(workload, plan_ids):
         return None
     rec = json.loads(text[a + 7:text.index("```", a + 7)])
     src_hash = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
-    if rec.get("workload") != workload or rec.get("plan_ids") != plan_ids or rec.get("attn_fwd_sha256") != src_hash:
+    order_hash = hashlib.sha256(open(ORDER_SRC, "rb").read()).hexdigest()
+    if rec.get("workload") != workload or rec.get("plan_ids") != plan_ids or rec.get("attn_fwd_sha256") != src_hash \
+            or rec.get("task_order_sha256") != order_hash:
         return None
     return rec["hbm_bytes_per_launch"]
 

@@ -39,10 +39,11 @@ def test_traffic_record_is_used_only_for_its_kernel_workload_and_plan():
     text = open(bench.TRAFFIC_FILE).read()
     rec = json.loads(text[text.index("```json") + 7:text.index("```", text.index("```json") + 7)])
     src = hashlib.sha256(open(bench.KERNEL_SRC, "rb").read()).hexdigest()
+    order = hashlib.sha256(open(bench.ORDER_SRC, "rb").read()).hexdigest()
     got = bench.measured_traffic(rec["workload"], rec["plan_ids"])
-    if rec["attn_fwd_sha256"] == src:
+    if rec["attn_fwd_sha256"] == src and rec.get("task_order_sha256") == order:
         assert got == rec["hbm_bytes_per_launch"] and got > 0
     else:
-        assert got is None   # the kernel changed since the counters were taken
+        assert got is None   # the kernel or the dispatch order changed since the counters were taken
     assert bench.measured_traffic(rec["workload"], [p + 1 for p in rec["plan_ids"]]) is None
     assert bench.measured_traffic("another_workload", rec["plan_ids"]) is None
