@@ -140,7 +140,10 @@ enum {
   BSA_EXPORT_TILE_PTR = 3,    /* segment's physical tile offsets, int64 [rows + 1] */
   BSA_EXPORT_TILE_KV = 4,     /* segment's physical KV tile index per active tile, int32 */
   BSA_EXPORT_TILE_MEMBER = 5, /* segment's membership bits per tile, uint64 (Coarsened plans) */
-  BSA_EXPORT_TASKS = 6        /* segment's tasks, int64 [n_tasks][6]: bh, pq, tile_begin, tile_end, split, nsplit */
+  BSA_EXPORT_TASKS = 6,       /* segment's tasks, int64 [n_tasks][6]: bh, pq, tile_begin, tile_end, split, nsplit */
+  BSA_EXPORT_DISPATCH = 7     /* segment's dispatch order, int64 [n_tasks]: the BSA_EXPORT_TASKS index of the task
+                                 at each position (row order, each task moved up to the first task with the same
+                                 KV tile list and member bits; the identity in row order) */
 };
 
 /* Library version. */

@@ -18,8 +18,8 @@ import numpy as np
 
 from . import _ffi
 from ._ffi import (BsaError, CatalogEntry, Mask, PlanOpts, RegimeQuery, SegmentInfo, Shapes,  # noqa: F401
-                   DTYPE_BF16, EXPORT_BH_NNZ, EXPORT_COL_IDX, EXPORT_ROW_PTR, EXPORT_TASKS, EXPORT_TILE_KV,
-                   EXPORT_TILE_MEMBER, EXPORT_TILE_PTR)
+                   DTYPE_BF16, EXPORT_BH_NNZ, EXPORT_COL_IDX, EXPORT_DISPATCH, EXPORT_ROW_PTR, EXPORT_TASKS,
+                   EXPORT_TILE_KV, EXPORT_TILE_MEMBER, EXPORT_TILE_PTR)
 
 _lib = _ffi.load()
 
@@ -193,7 +193,7 @@ class Plan:
     def export(self, what: int, segment: int = 0) -> np.ndarray:
         dtype = {EXPORT_ROW_PTR: np.int64, EXPORT_COL_IDX: np.int32, EXPORT_BH_NNZ: np.int64,
                  EXPORT_TILE_PTR: np.int64, EXPORT_TILE_KV: np.int32, EXPORT_TILE_MEMBER: np.uint64,
-                 EXPORT_TASKS: np.int64}[what]
+                 EXPORT_TASKS: np.int64, EXPORT_DISPATCH: np.int64}[what]
         need = ctypes.c_size_t()
         _check(_lib.bsa_plan_export(self.handle, segment, what, None, 0, ctypes.byref(need)))
         out = np.empty(need.value // np.dtype(dtype).itemsize, dtype=dtype)

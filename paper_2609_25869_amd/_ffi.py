@@ -16,7 +16,8 @@ c_i32, c_i64, c_sz, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctyp
 
 BSA_OK, BSA_ERR_INVALID, BSA_ERR_UNSUPPORTED, BSA_ERR_HIP, BSA_ERR_OOM, BSA_ERR_LUT = range(6)
 DTYPE_BF16, DTYPE_F16, DTYPE_F32 = 0, 1, 2
-EXPORT_ROW_PTR, EXPORT_COL_IDX, EXPORT_BH_NNZ, EXPORT_TILE_PTR, EXPORT_TILE_KV, EXPORT_TILE_MEMBER, EXPORT_TASKS = range(7)
+(EXPORT_ROW_PTR, EXPORT_COL_IDX, EXPORT_BH_NNZ, EXPORT_TILE_PTR, EXPORT_TILE_KV, EXPORT_TILE_MEMBER, EXPORT_TASKS,
+ EXPORT_DISPATCH) = range(8)
 MAX_SEGMENTS = 16
 
 

@@ -178,6 +178,7 @@ struct Segment {
   int64_t tasks_bound = 0;
   int32_t* order = nullptr;     // dispatch order of the tasks (Split-K plans); null: as stored
   Task* tasks_run = nullptr;    // the tasks in dispatch order (plans without Split-K); null: row order
+  int32_t* dispatch = nullptr;  // the dispatch order (exported); null: row order
   float* ws = nullptr;
   int64_t ws_bytes = 0;
 };
@@ -734,6 +735,7 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
       // row-order list stays for the plan export
       sg.tasks_run = oa.tasks_out;
       sg.order = e.split == 1 ? nullptr : oa.order;
+      sg.dispatch = oa.order;
     }
   }
   HIP_TRY(hipEventRecord(p->ready, stream));
@@ -939,6 +941,23 @@ bsa_status bsa_plan_export(bsa_plan_t plan, int32_t segment, int32_t what, void*
         const int64_t f[6] = {t[i].bh, t[i].pq, lo, hi, t[i].split, t[i].nsplit};
         std::memcpy(dst + 6 * i, f, sizeof f);
       }
+      return BSA_OK;
+    }
+    case BSA_EXPORT_DISPATCH: {
+      int64_t nt = sg.Rp;
+      if (sg.plan.split > 1 && (st = read_device_i64(plan, sg.task_ptr + sg.Rp, &nt)) != BSA_OK) return st;
+      *needed = sizeof(int64_t) * (size_t)nt;
+      if (!host_buf) return BSA_OK;
+      if (bytes < *needed) return fail(BSA_ERR_INVALID, "export buffer too small");
+      std::vector<int32_t> o((size_t)nt);
+      if (sg.dispatch && nt) {
+        HIP_TRY(hipMemcpyAsync(o.data(), sg.dispatch, sizeof(int32_t) * nt, hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipStreamSynchronize(s));
+      } else {
+        for (int64_t i = 0; i < nt; ++i) o[(size_t)i] = (int32_t)i;
+      }
+      int64_t* dst = static_cast<int64_t*>(host_buf);
+      for (int64_t i = 0; i < nt; ++i) dst[i] = o[(size_t)i];
       return BSA_OK;
     }
     default: return fail(BSA_ERR_INVALID, "unknown export selector");

@@ -70,3 +70,15 @@ def compare_lse(L_gpu: np.ndarray, L_ref: np.ndarray, what: str = "", tol: float
     if fin.any():
         rel = np.abs(L_gpu[fin] - L_ref[fin]) / np.maximum(1.0, np.abs(L_ref[fin]))
         assert rel.max() <= tol, "%s: LSE error %.3g" % (what, rel.max())
+
+
+def expected_dispatch(tasks: np.ndarray, tile_kv: np.ndarray, member: Optional[np.ndarray]) -> np.ndarray:
+    """The dispatch order the planner documents, from exported plan metadata:
+    row order, with every task moved up to the first task (in row order) of
+    the same (batch, head) that has the same KV tile list and member bits."""
+    first = {}
+    rep = []
+    for i, (bh, _pq, lo, hi, _s, _ns) in enumerate(np.asarray(tasks).tolist()):
+        mem = tuple(member[lo:hi].tolist()) if member is not None and len(member) else ()
+        rep.append(first.setdefault((bh, tuple(tile_kv[lo:hi].tolist()), mem), i))
+    return np.array(sorted(range(len(rep)), key=lambda i: (rep[i], i)), dtype=np.int64)

@@ -14,7 +14,7 @@ import pytest
 
 from oracle import attn as oattn
 from oracle import plans
-from tests.gpu_util import compare, compare_lse, log, run_plan
+from tests.gpu_util import compare, compare_lse, expected_dispatch, log, run_plan
 from workloads import CONFIGS, make_mask, make_qkv
 
 pytestmark = pytest.mark.gpu
@@ -77,8 +77,13 @@ def test_full_size_parity(name):
         assert np.array_equal(p.export(bsa.EXPORT_TILE_PTR, si), tiles.row_ptr)
         assert np.array_equal(p.export(bsa.EXPORT_TILE_KV, si), tiles.kv_tile)
         assert np.array_equal(p.export(bsa.EXPORT_TILE_MEMBER, si), tiles.member)
-        assert np.array_equal(p.export(bsa.EXPORT_TASKS, si), plans.split_tasks(tiles, info["split"]))
-    log("  planning state matches the enumeration (%d segments)" % len(segs))
+        tasks = plans.split_tasks(tiles, info["split"])
+        assert np.array_equal(p.export(bsa.EXPORT_TASKS, si), tasks)
+        want = np.arange(len(tasks))
+        if len(tasks) > 512:
+            want = expected_dispatch(tasks, tiles.kv_tile, tiles.member if len(tiles.member) else None)
+        assert np.array_equal(p.export(bsa.EXPORT_DISPATCH, si), want)
+    log("  planning state and dispatch order match the enumeration (%d segments)" % len(segs))
     p.destroy()
     del od, lsed
     gc.collect()

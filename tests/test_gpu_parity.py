@@ -10,7 +10,7 @@ import pytest
 
 from oracle import attn as oattn
 from oracle import brute, plans
-from tests.gpu_util import bf16_to_f64, compare, compare_lse, log, run_plan, to_dev_bf16
+from tests.gpu_util import bf16_to_f64, compare, compare_lse, expected_dispatch, log, run_plan, to_dev_bf16
 from workloads import BlockMask, bf16_bits_from_f32, random_case
 
 pytestmark = pytest.mark.gpu
@@ -366,7 +366,15 @@ def test_dispatch_order_does_not_change_the_output():
         log("dispatch order, plan %d" % pid)
         p1, o1, l1, _ = run_plan(bsa, mask, q, k, v, force_plan=pid)
         p2, o2, l2, _ = run_plan(bsa, mask, q, k, v, force_plan=pid, keep_row_order=True)
-        ordered += p1.info()["n_tasks"] > 512
+        n_tasks = p1.info()["n_tasks"]
+        ordered += n_tasks > 512
+        tasks = p1.export(bsa.EXPORT_TASKS)
+        want = np.arange(len(tasks))
+        if n_tasks > 512:
+            member = p1.export(bsa.EXPORT_TILE_MEMBER)
+            want = expected_dispatch(tasks, p1.export(bsa.EXPORT_TILE_KV), member if len(member) else None)
+        assert np.array_equal(p1.export(bsa.EXPORT_DISPATCH), want), "plan %d: dispatch order" % pid
+        assert np.array_equal(p2.export(bsa.EXPORT_DISPATCH), np.arange(len(tasks)))
         assert torch.equal(o1, o2) and torch.equal(l1, l2), "plan %d: the dispatch order changed the output" % pid
         compare(bf16_to_f64(o1), O_ref, "dispatch order plan %d" % pid)
         compare_lse(l1.cpu().numpy().astype(np.float64), L_ref, "dispatch order plan %d" % pid)
