@@ -93,12 +93,11 @@ struct OrderArgs {
   int64_t ntasks;             // exact count, or the bound when ntasks_dev is set
   const int32_t* tile_kv;
   const uint64_t* member;     // may be null
-  uint64_t* keys_in;          // list hashes
-  uint64_t* keys_out;
+  uint64_t* table_key;        // [table_size] list hashes (0: free slot)
+  int32_t* table_min;         // [table_size] lowest task index per hash
+  int64_t table_size;         // a power of two >= 2 * ntasks
+  int32_t* task_slot;         // table slot of each task
   int32_t* idx_in;
-  int32_t* idx_sorted;
-  int32_t* head_pos;
-  int32_t* head_run;
   uint32_t* rep;              // representative task of each task
   uint32_t* rep_sorted;
   int32_t* order;             // out; the first (device count) entries are the real tasks
@@ -139,6 +138,7 @@ hipError_t launch_task_count(const TaskArgs& a, hipStream_t s);
 hipError_t launch_task_fill(const TaskArgs& a, hipStream_t s);
 hipError_t launch_attention(int tq, int tkv, const AttnArgs& a, hipStream_t s);
 bool attention_variant_exists(int tq, int tkv);
+int64_t task_order_table_size(int64_t n);
 hipError_t task_order_temp_bytes(int64_t n, size_t* bytes);
 hipError_t launch_task_order(const OrderArgs& a, hipStream_t s);
 hipError_t launch_splitk_merge(int tq, const AttnArgs& a, hipStream_t s);

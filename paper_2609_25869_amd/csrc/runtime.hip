@@ -642,9 +642,9 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
     size_t order_temp = 0;
     if (ordered) HIP_TRY(task_order_temp_bytes(sg.tasks_bound, &order_temp));
     const size_t nb = ordered ? (size_t)sg.tasks_bound : 0;
-    const size_t o_kin = take(sizeof(uint64_t) * nb), o_kout = take(sizeof(uint64_t) * nb);
-    const size_t o_iin = take(sizeof(int32_t) * nb), o_isort = take(sizeof(int32_t) * nb);
-    const size_t o_hpos = take(sizeof(int32_t) * nb), o_hrun = take(sizeof(int32_t) * nb);
+    const int64_t table_size = ordered ? task_order_table_size(sg.tasks_bound) : 0;
+    const size_t o_tkey = take(sizeof(uint64_t) * (size_t)table_size), o_tmin = take(sizeof(int32_t) * (size_t)table_size);
+    const size_t o_slot = take(sizeof(int32_t) * nb), o_iin = take(sizeof(int32_t) * nb);
     const size_t o_rep = take(sizeof(uint32_t) * nb), o_rsort = take(sizeof(uint32_t) * nb);
     const size_t o_order = take(sizeof(int32_t) * nb);
     const size_t o_otemp = take(order_temp);
@@ -718,12 +718,11 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
       oa.ntasks = sg.tasks_bound;
       oa.tile_kv = sg.tile_kv;
       oa.member = sg.member;
-      oa.keys_in = reinterpret_cast<uint64_t*>(b8 + o_kin);
-      oa.keys_out = reinterpret_cast<uint64_t*>(b8 + o_kout);
+      oa.table_key = reinterpret_cast<uint64_t*>(b8 + o_tkey);
+      oa.table_min = reinterpret_cast<int32_t*>(b8 + o_tmin);
+      oa.table_size = table_size;
+      oa.task_slot = reinterpret_cast<int32_t*>(b8 + o_slot);
       oa.idx_in = reinterpret_cast<int32_t*>(b8 + o_iin);
-      oa.idx_sorted = reinterpret_cast<int32_t*>(b8 + o_isort);
-      oa.head_pos = reinterpret_cast<int32_t*>(b8 + o_hpos);
-      oa.head_run = reinterpret_cast<int32_t*>(b8 + o_hrun);
       oa.rep = reinterpret_cast<uint32_t*>(b8 + o_rep);
       oa.rep_sorted = reinterpret_cast<uint32_t*>(b8 + o_rsort);
       oa.order = reinterpret_cast<int32_t*>(b8 + o_order);

@@ -32,54 +32,60 @@ __device__ inline uint64_t mix64(uint64_t z) {
 
 constexpr int kWavesPerBlock = 4;
 
-// Key of task t: a hash of (bh, tile count, tile list, member bits), one
-// wave per task.  Entries past the device task count get the key ~0; the
-// representative pass keeps them behind every real task whatever their key.
+// Hash of task t's (bh, tile count, tile list, member bits), one wave per
+// task, entered into an open-addressing table that keeps, per distinct hash,
+// the lowest task index (the representative).  The probe loop is bounded by
+// the table size, which is at least twice the task count, so it always finds
+// a free or matching slot.
 __global__ __launch_bounds__(64 * kWavesPerBlock) void task_hash_kernel(OrderArgs a) {
   const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (t >= a.ntasks) return;
   const int64_t nt = a.ntasks_dev ? *a.ntasks_dev : a.ntasks;
-  uint64_t key = ~0ull;
-  if (t < nt) {
-    const Task tk = a.tasks[t];
-    const int64_t n = (int64_t)tk.tile_end - tk.tile_begin;
-    uint64_t h = 0;
-    for (int64_t i = lane; i < n; i += 64) {
-      const uint64_t kv = (uint32_t)a.tile_kv[tk.tile_begin + i];
-      const uint64_t mem = a.member ? a.member[tk.tile_begin + i] : 0ull;
-      h += mix64(kv | ((uint64_t)i << 32)) ^ mix64(mem + 0x9e3779b97f4a7c15ull * (uint64_t)(i + 1));
-    }
-    for (int off = 32; off > 0; off >>= 1) h += __shfl_xor(h, off);
-    key = mix64(h ^ mix64(((uint64_t)(uint32_t)tk.bh << 32) | (uint64_t)(uint32_t)n));
+  if (t >= nt) return;
+  const Task tk = a.tasks[t];
+  const int64_t n = (int64_t)tk.tile_end - tk.tile_begin;
+  uint64_t h = 0;
+  for (int64_t i = lane; i < n; i += 64) {
+    const uint64_t kv = (uint32_t)a.tile_kv[tk.tile_begin + i];
+    const uint64_t mem = a.member ? a.member[tk.tile_begin + i] : 0ull;
+    h += mix64(kv | ((uint64_t)i << 32)) ^ mix64(mem + 0x9e3779b97f4a7c15ull * (uint64_t)(i + 1));
   }
+  for (int off = 32; off > 0; off >>= 1) h += __shfl_xor(h, off);
+  h = mix64(h ^ mix64(((uint64_t)(uint32_t)tk.bh << 32) | (uint64_t)(uint32_t)n));
+  if (h == 0) h = 1;  // 0 marks a free slot
   if (lane == 0) {
-    a.keys_in[t] = key;
-    a.idx_in[t] = (int32_t)t;
+    const uint64_t mask = (uint64_t)a.table_size - 1;
+    uint64_t slot = h & mask;
+    for (int64_t probe = 0; probe < a.table_size; ++probe) {
+      const unsigned long long prev = atomicCAS(reinterpret_cast<unsigned long long*>(a.table_key + slot), 0ull,
+                                                (unsigned long long)h);
+      if (prev == 0ull || prev == h) {
+        atomicMin(a.table_min + slot, (int32_t)t);
+        a.task_slot[t] = (int32_t)slot;
+        break;
+      }
+      slot = (slot + 1) & mask;
+    }
   }
 }
 
-// Position p of the hash-sorted list: 1 + p where a run of equal keys starts, else 0.
-__global__ __launch_bounds__(256) void run_head_kernel(OrderArgs a) {
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= a.ntasks) return;
-  a.head_pos[p] = (p == 0 || a.keys_out[p] != a.keys_out[p - 1]) ? (int32_t)(p + 1) : 0;
-}
-
-// Representative of each task: the first task (lowest index) of its run of
-// equal keys; tasks past the device count represent themselves.
-__global__ __launch_bounds__(256) void representative_kernel(OrderArgs a) {
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= a.ntasks) return;
-  const int64_t nt = a.ntasks_dev ? *a.ntasks_dev : a.ntasks;
-  const int32_t t = a.idx_sorted[p];
-  const int32_t head = a.head_run[p] - 1;  // inclusive max-scan of run_head_kernel's output
-  a.rep[t] = t >= nt ? (uint32_t)t : (uint32_t)a.idx_sorted[head];
-}
-
-__global__ __launch_bounds__(256) void iota_kernel(int32_t* v, int64_t n) {
+__global__ __launch_bounds__(256) void table_clear_kernel(OrderArgs a) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) v[i] = (int32_t)i;
+  if (i >= a.table_size) return;
+  a.table_key[i] = 0ull;
+  a.table_min[i] = INT32_MAX;
+}
+
+// Representative of each task (tasks past the device count represent
+// themselves, so they sort behind every real task), and the identity as the
+// values of the sort.
+__global__ __launch_bounds__(256) void representative_kernel(OrderArgs a) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= a.ntasks) return;
+  const int64_t nt = a.ntasks_dev ? *a.ntasks_dev : a.ntasks;
+  a.rep[t] = t >= nt ? (uint32_t)t : (uint32_t)a.table_min[a.task_slot[t]];
+  a.idx_in[t] = (int32_t)t;
 }
 
 // The tasks themselves in dispatch order, so the kernel reads its task with
@@ -91,10 +97,6 @@ __global__ __launch_bounds__(256) void task_gather_kernel(OrderArgs a) {
   a.tasks_out[t] = a.tasks[a.order[t]];
 }
 
-struct MaxOp {
-  __device__ int32_t operator()(int32_t x, int32_t y) const { return x > y ? x : y; }
-};
-
 int rep_bits(int64_t n) {  // bits of the largest task index n - 1, at least 1
   int b = 1;
   while (b < 31 && (int64_t(1) << b) < n) ++b;
@@ -105,50 +107,34 @@ unsigned grid(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
 }  // namespace
 
+int64_t task_order_table_size(int64_t n) {
+  int64_t s = 1;
+  while (s < 2 * n) s <<= 1;
+  return s;
+}
+
 hipError_t task_order_temp_bytes(int64_t n, size_t* bytes) {
   *bytes = 0;
   if (n <= 1) return hipSuccess;
-  size_t b1 = 0, b2 = 0, b3 = 0;
-  hipError_t e = hipcub::DeviceRadixSort::SortPairs(nullptr, b1, static_cast<const uint64_t*>(nullptr),
-                                                    static_cast<uint64_t*>(nullptr),
-                                                    static_cast<const int32_t*>(nullptr),
-                                                    static_cast<int32_t*>(nullptr), (int)n, 0, 64, (hipStream_t)0);
-  if (e != hipSuccess) return e;
-  e = hipcub::DeviceScan::InclusiveScan(nullptr, b2, static_cast<const int32_t*>(nullptr),
-                                        static_cast<int32_t*>(nullptr), MaxOp(), (int)n, (hipStream_t)0);
-  if (e != hipSuccess) return e;
-  e = hipcub::DeviceRadixSort::SortPairs(nullptr, b3, static_cast<const uint32_t*>(nullptr),
-                                         static_cast<uint32_t*>(nullptr), static_cast<const int32_t*>(nullptr),
-                                         static_cast<int32_t*>(nullptr), (int)n, 0, rep_bits(n), (hipStream_t)0);
-  *bytes = std::max(b1, std::max(b2, b3));
-  return e;
+  return hipcub::DeviceRadixSort::SortPairs(nullptr, *bytes, static_cast<const uint32_t*>(nullptr),
+                                            static_cast<uint32_t*>(nullptr), static_cast<const int32_t*>(nullptr),
+                                            static_cast<int32_t*>(nullptr), (int)n, 0, rep_bits(n), (hipStream_t)0);
 }
 
 hipError_t launch_task_order(const OrderArgs& a, hipStream_t s) {
   const int64_t n = a.ntasks;
   if (n <= 1) return hipSuccess;
-  size_t bytes = a.temp_bytes;
-  // 1. hash every task's list; sort (hash, index) so equal lists form runs,
-  //    lowest index first (the sort is stable)
-  hipLaunchKernelGGL(task_hash_kernel, dim3(grid(n, kWavesPerBlock)), dim3(64 * kWavesPerBlock), 0, s, a);
+  // 1. representatives: the lowest task index per distinct list hash
+  hipLaunchKernelGGL(table_clear_kernel, dim3(grid(a.table_size, 256)), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = hipcub::DeviceRadixSort::SortPairs(a.temp, bytes, a.keys_in, a.keys_out, a.idx_in, a.idx_sorted, (int)n, 0, 64,
-                                         s);
-  if (e != hipSuccess) return e;
-  // 2. each task's representative: the first index of its run
-  hipLaunchKernelGGL(run_head_kernel, dim3(grid(n, 256)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(task_hash_kernel, dim3(grid(n, kWavesPerBlock)), dim3(64 * kWavesPerBlock), 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  bytes = a.temp_bytes;
-  e = hipcub::DeviceScan::InclusiveScan(a.temp, bytes, a.head_pos, a.head_run, MaxOp(), (int)n, s);
-  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(representative_kernel, dim3(grid(n, 256)), dim3(256), 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  // 3. order by (representative, index): row order with equal lists pulled
-  //    up to their first occurrence
-  hipLaunchKernelGGL(iota_kernel, dim3(grid(n, 256)), dim3(256), 0, s, a.idx_in, n);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  bytes = a.temp_bytes;
+  // 2. order by (representative, index): row order with equal lists pulled
+  //    up to their first occurrence (the radix sort is stable)
+  size_t bytes = a.temp_bytes;
   e = hipcub::DeviceRadixSort::SortPairs(a.temp, bytes, a.rep, a.rep_sorted, a.idx_in, a.order, (int)n, 0, rep_bits(n),
                                          s);
   if (e != hipSuccess || !a.tasks_out) return e;
