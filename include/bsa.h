@@ -90,9 +90,10 @@ typedef struct {
   int32_t force_plan;  /* >= 0: use this catalog plan for every segment (must be eligible); -1: select */
   int32_t select_mode; /* 0: plan table (Algorithm 2); 1: base plan only */
   bsa_lut_t lut;       /* NULL: the library's default table (BSA_LUT_PATH or the shipped artifact) */
-  int32_t keep_row_order; /* 0: dispatch the tasks of each head grouped by their KV tile range, so
-                             tasks that read the same K/V run side by side and share the L2;
-                             1: dispatch them in row order.  The output is the same either way. */
+  int32_t keep_row_order; /* 0: above 512 tasks, dispatch in row order except that each task moves up
+                             to the first task of its head with the same KV tile list, so tasks that
+                             read the same K/V run side by side and share the L2 (BSA_EXPORT_DISPATCH);
+                             1: dispatch in row order.  The output is the same either way. */
 } bsa_plan_opts;
 
 /* Per-segment summary of a plan.  Heads that share one logical geometry form

@@ -212,8 +212,8 @@ def plan(mask, bq: Union[int, Sequence[int]], bkv: Union[int, Sequence[int]], sh
          select_mode: int = 0, lut: Optional[Lut] = None, stream=None, keep_row_order: bool = False) -> Plan:
     """Plan a request (bsa_plan).  `mask` is a CUDA uint8/bool tensor holding the
     logical block masks; see include/bsa.h for its layout.  keep_row_order
-    dispatches the tasks in row order instead of grouped by KV tile range
-    (same output)."""
+    dispatches the tasks in row order instead of with equal KV tile lists
+    side by side (same output)."""
     import torch
     if not (isinstance(mask, torch.Tensor) and mask.is_cuda and mask.dtype in (torch.uint8, torch.bool)):
         raise TypeError("mask must be a CUDA uint8 or bool tensor")
