@@ -57,16 +57,18 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void task_hash_kernel(OrderArg
   if (lane == 0) {
     const uint64_t mask = (uint64_t)a.table_size - 1;
     uint64_t slot = h & mask;
+    int32_t found = -1;  // stays -1 only if the table were full, which its size rules out
     for (int64_t probe = 0; probe < a.table_size; ++probe) {
       const unsigned long long prev = atomicCAS(reinterpret_cast<unsigned long long*>(a.table_key + slot), 0ull,
                                                 (unsigned long long)h);
       if (prev == 0ull || prev == h) {
         atomicMin(a.table_min + slot, (int32_t)t);
-        a.task_slot[t] = (int32_t)slot;
+        found = (int32_t)slot;
         break;
       }
       slot = (slot + 1) & mask;
     }
+    a.task_slot[t] = found;
   }
 }
 
@@ -84,7 +86,8 @@ __global__ __launch_bounds__(256) void representative_kernel(OrderArgs a) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= a.ntasks) return;
   const int64_t nt = a.ntasks_dev ? *a.ntasks_dev : a.ntasks;
-  a.rep[t] = t >= nt ? (uint32_t)t : (uint32_t)a.table_min[a.task_slot[t]];
+  const int32_t slot = t < nt ? a.task_slot[t] : -1;
+  a.rep[t] = slot < 0 ? (uint32_t)t : (uint32_t)a.table_min[slot];
   a.idx_in[t] = (int32_t)t;
 }
 
