@@ -112,9 +112,13 @@ def test_library_lookup_matches_the_regions(tmp_path):
         feats = {"seq_q": z.seq_q, "batch_heads": z.batch_heads, "nnz": nnz, "blocks": blocks,
                  "run_blocks": z.run_blocks}
         key = (bq, bkv, 0, 128)
-        want, hit = tree.select(regions, key, feats, base(key))
+        # Algorithm 2's lookup over the key's regions, by the oracle's leaf test
+        leaves = [(region, ranking) for region, ranking, _ in regions.get(key, {}).get("regimes", [])]
+        want, hit = regime.lookup_regions(leaves, oracle_features(feats), tree.FEATURES, base(key))
+        assert sum(regime.region_contains(oracle_features(feats), r, tree.FEATURES) for r, _ in leaves) <= 1
         got, ghit = bsa.lut_rank(z, lut)
         assert (got, ghit) == (want, hit), (t, key, feats)
+        assert tree.select(regions, key, feats, base(key)) == (want, hit)
     lut.close()
 
 
