@@ -261,6 +261,26 @@ BSA_API bsa_status bsa_plan_destroy(bsa_plan_t plan);
 BSA_API bsa_status bsa_sparsify_topk(const void* q, const void* k, const bsa_shapes* shapes, int32_t bq,
                                      int32_t bkv, int32_t topk, int32_t diagonal, uint8_t* mask, void* stream);
 
+/*
+ * bsa_sparsify_topk without any device allocation, for callers that cannot
+ * allocate: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Arguments, layouts, the selection and its error codes
+ * are those of bsa_sparsify_topk; the result is the same mask bit for bit.
+ * Its block means and score rows live in a fixed 64 MiB scratch array that
+ * the library keeps on every device it runs on until the process ends
+ * (looked up once per device).  One pass holds as many heads as fit, so the
+ * limit is one head: (ceil(seq_q/bq) + ceil(seq_kv/bkv)) * 1024 bytes of
+ * means plus ceil(seq_q/bq) * ceil(seq_kv/bkv) * 8 bytes of scores must not
+ * exceed 64 MiB (BSA_ERR_INVALID otherwise, before any device work).  Every
+ * call on a device shares that device's scratch and leaves its contents
+ * behind: calls that overlap in time on one device (different streams or
+ * threads) race and must be serialised by the caller.  Asynchronous on
+ * `stream`; calls no hipMalloc, hipFree or allocating library routine.
+ */
+BSA_API bsa_status bsa_sparsify_topk_noalloc(const void* q, const void* k, const bsa_shapes* shapes, int32_t bq,
+                                             int32_t bkv, int32_t topk, int32_t diagonal, uint8_t* mask,
+                                             void* stream);
+
 #ifdef __cplusplus
 }
 #endif

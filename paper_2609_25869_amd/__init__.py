@@ -252,11 +252,15 @@ def forward(p: Plan, q, k, v, o, lse=None, stream=None):
     return o
 
 
-def sparsify_topk(q, k, bq: int, bkv: int, topk: int, diagonal: bool = True, mask=None, stream=None):
+def sparsify_topk(q, k, bq: int, bkv: int, topk: int, diagonal: bool = True, mask=None, stream=None,
+                  noalloc: bool = False):
     """Mean-pooled top-k block mask of bf16 [B, N, H, 128] tensors q and k
     (bsa_sparsify_topk): uint8 [B, H, ceil(Nq / bq), ceil(Nkv / bkv)] on the
     device, written into `mask` when given.  Pass it to plan() with
-    head_offset = [h * nqb * nkb] and stride_b = H * nqb * nkb."""
+    head_offset = [h * nqb * nkb] and stride_b = H * nqb * nkb.  With
+    noalloc=True the library's allocation-free entry point
+    (bsa_sparsify_topk_noalloc) runs instead; pass `mask` to allocate
+    nothing at all."""
     import torch
     for t in (q, k):
         if not t.is_cuda or t.dtype != torch.bfloat16 or t.dim() != 4 or t.stride(3) != 1:
@@ -273,7 +277,7 @@ def sparsify_topk(q, k, bq: int, bkv: int, topk: int, diagonal: bool = True, mas
         raise ValueError("mask must be a contiguous CUDA uint8 tensor of shape %s" % ((B, H, nqb, nkb),))
     st = lambda t: (t.stride(0), t.stride(2), t.stride(1))
     shapes = make_shapes(B, H, Nq, Nkv, d, st(q), st(k), st(k), st(q))
-    _check(_lib.bsa_sparsify_topk(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()), ctypes.byref(shapes),
-                                  int(bq), int(bkv), int(topk), 1 if diagonal else 0, ctypes.c_void_p(mask.data_ptr()),
-                                  _stream_handle(stream)))
+    fn = _lib.bsa_sparsify_topk_noalloc if noalloc else _lib.bsa_sparsify_topk
+    _check(fn(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()), ctypes.byref(shapes), int(bq), int(bkv),
+              int(topk), 1 if diagonal else 0, ctypes.c_void_p(mask.data_ptr()), _stream_handle(stream)))
     return mask

@@ -79,6 +79,8 @@ SIGNATURES = [
     ("bsa_plan_export", c_i32, [c_vp, c_i32, c_i32, c_vp, c_sz, ctypes.POINTER(c_sz)]),
     ("bsa_plan_destroy", c_i32, [c_vp]),
     ("bsa_sparsify_topk", c_i32, [c_vp, c_vp, ctypes.POINTER(Shapes), c_i32, c_i32, c_i32, c_i32, c_vp, c_vp]),
+    ("bsa_sparsify_topk_noalloc", c_i32, [c_vp, c_vp, ctypes.POINTER(Shapes), c_i32, c_i32, c_i32, c_i32, c_vp,
+                                          c_vp]),
 ]
 
 

@@ -968,8 +968,11 @@ bsa_status bsa_plan_destroy(bsa_plan_t plan) {
   return BSA_OK;
 }
 
-bsa_status bsa_sparsify_topk(const void* q, const void* k, const bsa_shapes* shapes, int32_t bq, int32_t bkv,
-                             int32_t topk, int32_t diagonal, uint8_t* mask, void* stream_in) {
+namespace {
+
+// Checks shared by both sparsifier entry points; fills the block grid.
+bsa_status sparsify_validate(const void* q, const void* k, const bsa_shapes* shapes, int32_t bq, int32_t bkv,
+                             uint8_t* mask, int64_t* nqb, int64_t* nkb) {
   if (!q || !k || !mask) return fail(BSA_ERR_INVALID, "q, k and mask must be device pointers");
   bsa_status st = validate_shapes(shapes);
   if (st != BSA_OK) return st;
@@ -977,25 +980,29 @@ bsa_status bsa_sparsify_topk(const void* q, const void* k, const bsa_shapes* sha
   const bsa_shapes& s = *shapes;
   if (s.dtype != BSA_DTYPE_BF16) return fail(BSA_ERR_UNSUPPORTED, "only bfloat16 tensors are implemented");
   if (s.head_dim != kHeadDim) return fail(BSA_ERR_UNSUPPORTED, "only head_dim 128 is implemented");
-  const int64_t nqb = cdiv(s.seq_q, bq), nkb = cdiv(s.seq_kv, bkv);
-  if (nkb > sparsify_max_kv_blocks())
+  *nqb = cdiv(s.seq_q, bq);
+  *nkb = cdiv(s.seq_kv, bkv);
+  if (*nkb > sparsify_max_kv_blocks())
     return fail(BSA_ERR_UNSUPPORTED, "more than " + std::to_string(sparsify_max_kv_blocks()) + " KV blocks per row");
-  hipStream_t stream = (hipStream_t)stream_in;
-  int dev = 0;
-  HIP_TRY(hipGetDevice(&dev));
-  prepare_pool(dev);
+  return BSA_OK;
+}
+
+// Device bytes of one head's block means (queries and keys) and score rows.
+int64_t sparsify_head_bytes(int64_t nqb, int64_t nkb) {
+  return (nqb + nkb) * kHeadDim * (int64_t)sizeof(double) + nqb * nkb * (int64_t)sizeof(double);
+}
+
+// The sparsifier's passes over the heads, `chunk` heads at a time, with the
+// block means and score rows of a pass in `work` (at least chunk * head bytes).
+hipError_t sparsify_passes(const void* q, const void* k, const bsa_shapes& s, int32_t bq, int32_t bkv, int32_t topk,
+                           int32_t diagonal, uint8_t* mask, int64_t nqb, int64_t nkb, int64_t chunk, void* work,
+                           hipStream_t stream) {
   const int64_t nbh = (int64_t)s.batch * s.heads;
-  // heads per pass: score rows of at most 256 MiB
-  const int64_t per_head = nqb * nkb * (int64_t)sizeof(double);
-  const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(nbh, (int64_t(256) << 20) / per_head));
   const size_t bytes_q = (size_t)(chunk * nqb * kHeadDim) * sizeof(double);
   const size_t bytes_k = (size_t)(chunk * nkb * kHeadDim) * sizeof(double);
-  const size_t bytes_s = (size_t)(chunk * per_head);
-  void* scratch = nullptr;
-  HIP_TRY(hipMallocAsync(&scratch, bytes_q + bytes_k + bytes_s, stream));
-  double* pq = static_cast<double*>(scratch);
-  double* pk = reinterpret_cast<double*>(static_cast<uint8_t*>(scratch) + bytes_q);
-  double* sc = reinterpret_cast<double*>(static_cast<uint8_t*>(scratch) + bytes_q + bytes_k);
+  double* pq = static_cast<double*>(work);
+  double* pk = reinterpret_cast<double*>(static_cast<uint8_t*>(work) + bytes_q);
+  double* sc = reinterpret_cast<double*>(static_cast<uint8_t*>(work) + bytes_q + bytes_k);
   const uint16_t* qh = static_cast<const uint16_t*>(q);
   const uint16_t* kh = static_cast<const uint16_t*>(k);
   hipError_t e = hipSuccess;
@@ -1011,9 +1018,85 @@ bsa_status bsa_sparsify_topk(const void* q, const void* k, const bsa_shapes* sha
       e = launch_topk_select(sc, (int32_t)nqb, (int32_t)nkb, topk, diagonal ? 1 : 0, s.seq_q, s.seq_kv, bq, bkv,
                              (int32_t)bh0, n, mask, stream);
   }
-  const hipError_t ef = hipFreeAsync(scratch, stream);
+  return e;
+}
+
+// Scratch of the allocation-free sparsifier: one copy per device, resident
+// until the process ends.  Host code never passes `scratch` itself to a
+// kernel (in host code it names a host-side stand-in); it uses the device
+// address that hipGetSymbolAddress returns for the current device.
+constexpr int64_t kNoAllocScratchBytes = int64_t(64) << 20;
+static __device__ __attribute__((aligned(256))) uint8_t scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on device `dev` (looked up once per device,
+// with that device current).
+bsa_status scratch_address(int dev, void** out) {
+  *out = nullptr;
+  if (dev < 0 || dev >= kMaxDevices) return fail(BSA_ERR_UNSUPPORTED, "device index beyond the scratch table");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(BSA_ERR_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return BSA_OK;
+}
+
+}  // namespace
+
+bsa_status bsa_sparsify_topk(const void* q, const void* k, const bsa_shapes* shapes, int32_t bq, int32_t bkv,
+                             int32_t topk, int32_t diagonal, uint8_t* mask, void* stream_in) {
+  int64_t nqb = 0, nkb = 0;
+  bsa_status st = sparsify_validate(q, k, shapes, bq, bkv, mask, &nqb, &nkb);
+  if (st != BSA_OK) return st;
+  const bsa_shapes& s = *shapes;
+  hipStream_t stream = (hipStream_t)stream_in;
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  prepare_pool(dev);
+  const int64_t nbh = (int64_t)s.batch * s.heads;
+  // heads per pass: score rows of at most 256 MiB
+  const int64_t per_scores = nqb * nkb * (int64_t)sizeof(double);
+  const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(nbh, (int64_t(256) << 20) / per_scores));
+  void* work = nullptr;
+  HIP_TRY(hipMallocAsync(&work, (size_t)(chunk * sparsify_head_bytes(nqb, nkb)), stream));
+  const hipError_t e = sparsify_passes(q, k, s, bq, bkv, topk, diagonal, mask, nqb, nkb, chunk, work, stream);
+  const hipError_t ef = hipFreeAsync(work, stream);
   if (e != hipSuccess) return fail(BSA_ERR_HIP, std::string("sparsifier launch: ") + hipGetErrorString(e));
   if (ef != hipSuccess) return fail(BSA_ERR_HIP, std::string("hipFreeAsync: ") + hipGetErrorString(ef));
+  return BSA_OK;
+}
+
+bsa_status bsa_sparsify_topk_noalloc(const void* q, const void* k, const bsa_shapes* shapes, int32_t bq,
+                                     int32_t bkv, int32_t topk, int32_t diagonal, uint8_t* mask, void* stream_in) {
+  int64_t nqb = 0, nkb = 0;
+  bsa_status st = sparsify_validate(q, k, shapes, bq, bkv, mask, &nqb, &nkb);
+  if (st != BSA_OK) return st;
+  const int64_t per_head = sparsify_head_bytes(nqb, nkb);
+  if (per_head > kNoAllocScratchBytes)
+    return fail(BSA_ERR_INVALID, "one head needs " + std::to_string(per_head) +
+                                     " bytes of block means and scores, more than the " +
+                                     std::to_string(kNoAllocScratchBytes) + "-byte scratch of this entry point");
+  const bsa_shapes& s = *shapes;
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  void* work = nullptr;
+  if ((st = scratch_address(dev, &work)) != BSA_OK) return st;
+  const int64_t nbh = (int64_t)s.batch * s.heads;
+  const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(nbh, kNoAllocScratchBytes / per_head));
+  // every byte of the scratch that a pass reads is written earlier in the
+  // same pass (means before scores, scores before the selection), so nothing
+  // needs clearing
+  const hipError_t e =
+      sparsify_passes(q, k, s, bq, bkv, topk, diagonal, mask, nqb, nkb, chunk, work, (hipStream_t)stream_in);
+  if (e != hipSuccess) return fail(BSA_ERR_HIP, std::string("sparsifier launch: ") + hipGetErrorString(e));
   return BSA_OK;
 }
 

@@ -35,7 +35,7 @@ def test_header_declares_the_request_entry_points():
     for required in ("bsa_plan", "bsa_forward", "bsa_plan_destroy", "bsa_lut_load", "bsa_plan_export",
                      "bsa_plan_info", "bsa_status_string", "bsa_last_error", "bsa_sparsify_topk"):
         assert required in names
-    assert len(names) == 19
+    assert len(names) == 20
 
 
 def test_library_exports_exactly_the_header():
