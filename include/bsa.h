@@ -48,7 +48,7 @@ extern "C" {
 #define BSA_API __attribute__((visibility("default")))
 
 #define BSA_VERSION_MAJOR 1
-#define BSA_VERSION_MINOR 0
+#define BSA_VERSION_MINOR 1
 #define BSA_MAX_SEGMENTS 16
 
 typedef enum {
@@ -116,13 +116,18 @@ typedef struct {
   int64_t workspace_bytes;   /* Split-K partial-state workspace */
 } bsa_segment_info;
 
-/* One catalog entry (Section 4.4): a native kernel configuration. */
+/* One catalog entry (Section 4.4): a native kernel configuration, i.e. a
+ * physical tile (Section 4.2) and a task organization (Section 4.3). */
 typedef struct {
   int32_t id;
   int32_t tq, tkv;   /* physical tile */
   int32_t split;     /* Split-K partitions per query tile (1 = none) */
   int32_t stages;    /* pipeline depth (buffered K/V stages) */
   int32_t waves;     /* wavefronts per workgroup */
+  int32_t xcd_group; /* traversal order: the MI355X's eight XCDs work in groups of this many (2 or 8), each
+                        group through its own contiguous share of the dispatch order, the XCDs of a group
+                        taking turns over runs of 8 consecutive tasks; 8 keeps every XCD on the same stretch
+                        of tasks (the same heads), 2 spreads four stretches over the chip */
 } bsa_catalog_entry;
 
 /* Regime-lookup input z_A(R) = <k_A(R), u_A(R), s_A(M)> (Eq. 3). */

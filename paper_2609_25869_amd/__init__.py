@@ -81,7 +81,8 @@ def catalog() -> List[Dict[str, int]]:
     e = CatalogEntry()
     for i in range(_lib.bsa_catalog_size()):
         _check(_lib.bsa_catalog_get(i, ctypes.byref(e)))
-        out.append(dict(id=e.id, tq=e.tq, tkv=e.tkv, split=e.split, stages=e.stages, waves=e.waves))
+        out.append(dict(id=e.id, tq=e.tq, tkv=e.tkv, split=e.split, stages=e.stages, waves=e.waves,
+                        xcd_group=e.xcd_group))
     return out
 
 

@@ -46,7 +46,7 @@ class SegmentInfo(ctypes.Structure):
 
 class CatalogEntry(ctypes.Structure):
     _fields_ = [("id", c_i32), ("tq", c_i32), ("tkv", c_i32), ("split", c_i32), ("stages", c_i32),
-                ("waves", c_i32)]
+                ("waves", c_i32), ("xcd_group", c_i32)]
 
 
 class RegimeQuery(ctypes.Structure):

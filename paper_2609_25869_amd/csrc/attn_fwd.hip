@@ -118,14 +118,29 @@ struct Cfg {
   static constexpr int kTileBytes = TKV * kRowBytes;
 };
 
-// Map the launch slot to a task so that each XCD (slot % 8) walks its own
-// contiguous range of the task list.
-__device__ inline int64_t task_of_slot(int64_t slot, int64_t nt) {
-  const int64_t per = (nt + 7) / 8;
+// Map the launch slot to a task.  Slot i runs on XCD i % 8.  The XCDs form
+// 8 / group groups of `group` XCDs; group g works through the g-th contiguous
+// share of the task list, and inside it its XCDs take turns over runs of
+// `run` consecutive tasks (XCD member m takes runs m, m + group, ...), so
+// neighbouring tasks still share an XCD while the group's XCDs stay on the
+// same stretch of the list.  group = 1 gives each XCD its own contiguous
+// eighth; group = 8 keeps all XCDs on one stretch.  The tail of a share that
+// does not fill whole rounds of runs is dealt out one task per XCD.  Slots
+// map one-to-one onto [0, nt), the rest to -1.
+__device__ inline int64_t task_of_slot(int64_t slot, int64_t nt, int64_t group, int64_t run) {
   const int64_t xcd = slot & 7, local = slot >> 3;
-  if (local >= per) return -1;
-  const int64_t t = xcd * per + local;
-  return t < nt ? t : -1;
+  if (group <= 1) {
+    const int64_t per = (nt + 7) / 8;
+    const int64_t t = xcd * per + local;
+    return (local < per && t < nt) ? t : -1;
+  }
+  const int64_t ngroups = 8 / group, gi = xcd / group, mi = xcd % group;
+  const int64_t per = (nt + ngroups - 1) / ngroups;
+  const int64_t lo = gi * per, n = min(nt, lo + per) - lo;
+  const int64_t whole = n / (group * run);  // complete rounds of runs
+  const int64_t t = local < whole * run ? (local / run) * group * run + mi * run + local % run
+                                        : whole * group * run + (local - whole * run) * group + mi;
+  return t < n ? lo + t : -1;
 }
 
 // Value of the same register in lane l ^ 32 (the other half of the wave).
@@ -237,7 +252,7 @@ void attn_fwd_kernel(AttnArgs a) {
   auto vslot = [&](int i) -> uint8_t* { return kslot(i) + C::kTileBytes; };
 
   const int64_t nt = a.ntasks_dev ? *a.ntasks_dev : a.ntasks;
-  int64_t ti = task_of_slot(blockIdx.x, nt);
+  int64_t ti = task_of_slot(blockIdx.x, nt, a.slot_group, a.slot_run);
   if (ti < 0) return;
   if (a.order) ti = ((const __attribute__((address_space(4))) int32_t*)a.order)[ti];
   const Task task = a.tasks[ti];
@@ -791,38 +806,29 @@ __global__ __launch_bounds__(256) void splitk_merge_kernel(AttnArgs a) {
   }
 }
 
-// Ring depth per KV tile: with two waves per SIMD, four slots for 32-key
-// tiles and two for 64-key tiles (64 KB of LDS per workgroup, two
-// workgroups per CU); a 64-row-per-wave workgroup has the CU to itself and
-// takes eight slots (128 KB), so its loads have six iterations to land.
-constexpr int stages_for(int tkv, int g) { return g == 2 ? 8 : tkv == 32 ? 4 : 2; }
-
-template <int NWAVES, int G, int TKV>
+template <int NWAVES, int G, int TKV, int STAGES>
 hipError_t launch_variant(const AttnArgs& a, hipStream_t s) {
   const int64_t slots = ((int64_t)a.ntasks + 7) / 8 * 8;
   if (slots == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_fwd_kernel<NWAVES, G, TKV, stages_for(TKV, G)>), dim3((unsigned)slots),
-                     dim3(64 * NWAVES), 0, s, a);
+  hipLaunchKernelGGL((attn_fwd_kernel<NWAVES, G, TKV, STAGES>), dim3((unsigned)slots), dim3(64 * NWAVES), 0, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-bool attention_variant_exists(int tq, int tkv) {
-  return (tq == 64 || tq == 128 || tq == 256) && (tkv == 32 || tkv == 64);
-}
-
-// Kernel per physical tile shape.  T_Q = 256 with 32-key tiles runs four
-// waves of 64 rows (two row groups sharing every K and V operand); with
-// 64-key tiles the two groups' score and probability registers do not fit
-// beside the accumulators, and eight waves of 32 rows run instead.
-hipError_t launch_attention(int tq, int tkv, const AttnArgs& a, hipStream_t s) {
-  if (tq == 64 && tkv == 32) return launch_variant<2, 1, 32>(a, s);
-  if (tq == 64 && tkv == 64) return launch_variant<2, 1, 64>(a, s);
-  if (tq == 128 && tkv == 32) return launch_variant<4, 1, 32>(a, s);
-  if (tq == 128 && tkv == 64) return launch_variant<4, 1, 64>(a, s);
-  if (tq == 256 && tkv == 32) return launch_variant<4, 2, 32>(a, s);
-  if (tq == 256 && tkv == 64) return launch_variant<8, 1, 64>(a, s);
+// The kernel of a catalog entry: physical tile, wavefronts per workgroup and
+// ring depth (Section 4.4).  With two waves per SIMD a workgroup may use
+// 64 KB of LDS (two per CU): four slots of 32-key tiles or two of 64-key
+// tiles.  T_Q = 256 with 32-key tiles runs four waves of 64 rows (two row
+// groups sharing every K and V operand, one workgroup per CU, eight slots);
+// with 64-key tiles eight waves of 32 rows.
+hipError_t launch_attention(int tq, int tkv, int waves, int stages, const AttnArgs& a, hipStream_t s) {
+  if (tq == 64 && tkv == 32 && waves == 2 && stages == 4) return launch_variant<2, 1, 32, 4>(a, s);
+  if (tq == 64 && tkv == 64 && waves == 2 && stages == 2) return launch_variant<2, 1, 64, 2>(a, s);
+  if (tq == 128 && tkv == 32 && waves == 4 && stages == 4) return launch_variant<4, 1, 32, 4>(a, s);
+  if (tq == 128 && tkv == 64 && waves == 4 && stages == 2) return launch_variant<4, 1, 64, 2>(a, s);
+  if (tq == 256 && tkv == 32 && waves == 4 && stages == 8) return launch_variant<4, 2, 32, 8>(a, s);
+  if (tq == 256 && tkv == 64 && waves == 8 && stages == 2) return launch_variant<8, 1, 64, 2>(a, s);
   return hipErrorInvalidValue;
 }
 

@@ -125,6 +125,7 @@ struct AttnArgs {
   int32_t bq_shift, bkv_shift;  // log2 of the logical block sizes
   int32_t gq, gkv;              // membership grid of a tile
   float scale_log2;             // log2(e) / sqrt(d)
+  int32_t slot_group, slot_run; // launch-slot to task map: XCDs per group (1, 2, 4 or 8) and run length
 };
 
 // Kernel launchers (defined in the .hip files).
@@ -136,8 +137,7 @@ hipError_t launch_map_count(const MapArgs& a, hipStream_t s);
 hipError_t launch_map_fill(const MapArgs& a, hipStream_t s);
 hipError_t launch_task_count(const TaskArgs& a, hipStream_t s);
 hipError_t launch_task_fill(const TaskArgs& a, hipStream_t s);
-hipError_t launch_attention(int tq, int tkv, const AttnArgs& a, hipStream_t s);
-bool attention_variant_exists(int tq, int tkv);
+hipError_t launch_attention(int tq, int tkv, int waves, int stages, const AttnArgs& a, hipStream_t s);
 int64_t task_order_table_size(int64_t n);
 hipError_t task_order_temp_bytes(int64_t n, size_t* bytes);
 hipError_t launch_task_order(const OrderArgs& a, hipStream_t s);

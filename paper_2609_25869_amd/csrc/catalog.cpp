@@ -12,19 +12,30 @@ namespace bsa {
 
 namespace {
 
+// Ring depth and wavefronts of the kernel that runs tile (tq, tkv) with one
+// wave per 32 query rows (64 rows per wave for (256, 32)).
+int32_t default_stages(int tq, int tkv) { return (tq == 256 && tkv == 32) ? 8 : tkv == 32 ? 4 : 2; }
+int32_t default_waves(int tq, int tkv) { return (tq == 256 && tkv == 32) ? 4 : tq / 32; }
+
 std::vector<CatalogEntry> build_catalog() {
-  // id = ((tq index) * 2 + tkv index) * 4 + split index; 32-key tiles use a
-  // four-slot K/V ring, 64-key tiles a two-slot ring (same LDS footprint)
   const int tqs[] = {64, 128, 256};
   const int tkvs[] = {32, 64};
   const int splits[] = {1, 2, 4, 8};
   std::vector<CatalogEntry> out;
   int id = 0;
+  // ids 0-23: ((tq index) * 2 + tkv index) * 4 + split index, XCD pairs
   for (int tq : tqs)
     for (int tkv : tkvs)
-      for (int s : splits) out.push_back(CatalogEntry{id++, tq, tkv, s, tkv == 32 ? 4 : 2, tq / 32});
+      for (int s : splits) out.push_back(CatalogEntry{id++, tq, tkv, s, default_stages(tq, tkv), default_waves(tq, tkv), 2});
+  // ids 24-29: the split-free tiles with every XCD on the same stretch of tasks
+  for (int tq : tqs)
+    for (int tkv : tkvs) out.push_back(CatalogEntry{id++, tq, tkv, 1, default_stages(tq, tkv), default_waves(tq, tkv), 8});
   return out;
 }
+
+}  // namespace
+
+namespace {
 
 bool nests(int32_t t, int32_t b) { return t > 0 && b > 0 && (t % b == 0 || b % t == 0); }
 
@@ -307,9 +318,10 @@ bool lut_parse(const std::string& text, Lut* out, std::string* err) {
   }
   for (size_t k = 0; k < cat->arr.size(); ++k) {
     std::vector<int64_t> e;
-    if (!as_int_list(&cat->arr[k], &e) || e.size() != 6) { *err = "bad catalog entry"; return false; }
+    if (!as_int_list(&cat->arr[k], &e) || e.size() != 7) { *err = "bad catalog entry"; return false; }
     const CatalogEntry& c = catalog()[k];
-    if (e[0] != c.id || e[1] != c.tq || e[2] != c.tkv || e[3] != c.split || e[4] != c.stages || e[5] != c.waves) {
+    if (e[0] != c.id || e[1] != c.tq || e[2] != c.tkv || e[3] != c.split || e[4] != c.stages || e[5] != c.waves ||
+        e[6] != c.xcd_group) {
       *err = "artifact catalog entry " + std::to_string(k) + " does not match this library";
       return false;
     }

@@ -10,9 +10,12 @@
 
 namespace bsa {
 
-// Catalog of gfx950 plans (Section 4.4): physical tile x Split-K partitions.
+// Catalog of gfx950 plans (Section 4.4): a physical tile (the mapping of
+// Section 4.2) and an organization (Section 4.3): Split-K partitions, the
+// kernel's wavefronts and ring depth, and the traversal order of the tasks
+// over the eight XCDs (xcd_group XCDs share one stretch of the task list).
 struct CatalogEntry {
-  int32_t id, tq, tkv, split, stages, waves;
+  int32_t id, tq, tkv, split, stages, waves, xcd_group;
 };
 
 const std::vector<CatalogEntry>& catalog();

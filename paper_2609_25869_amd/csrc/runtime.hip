@@ -55,6 +55,10 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 // Task count above which the planner sorts a segment's tasks into KV order.
 constexpr int64_t kOrderMinTasks = 512;
 
+// Length of the runs of consecutive tasks that the XCDs of one group take
+// turns over (see the plan's traversal order, CatalogEntry::xcd_group).
+constexpr int32_t kSlotRun = 8;
+
 // ---------------------------------------------------------------------------
 // Pinned staging for the per-request host<->device copies.  One buffer per
 // process, reused; the lock is held from the upload until the request's one
@@ -399,7 +403,7 @@ int32_t bsa_catalog_size(void) { return (int32_t)catalog().size(); }
 bsa_status bsa_catalog_get(int32_t id, bsa_catalog_entry* out) {
   const CatalogEntry* e = catalog_find(id);
   if (!e || !out) return fail(BSA_ERR_INVALID, "bad catalog id or null output");
-  *out = bsa_catalog_entry{e->id, e->tq, e->tkv, e->split, e->stages, e->waves};
+  *out = bsa_catalog_entry{e->id, e->tq, e->tkv, e->split, e->stages, e->waves, e->xcd_group};
   return BSA_OK;
 }
 
@@ -781,7 +785,9 @@ bsa_status bsa_forward(bsa_plan_t plan, const void* q, const void* k, const void
     a.gq = sg.gq;
     a.gkv = sg.gkv;
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)s.head_dim));
-    HIP_TRY(launch_attention(e.tq, e.tkv, a, stream));
+    a.slot_group = e.xcd_group;
+    a.slot_run = kSlotRun;
+    HIP_TRY(launch_attention(e.tq, e.tkv, e.waves, e.stages, a, stream));
     if (e.split > 1) HIP_TRY(launch_splitk_merge(e.tq, a, stream));
   }
   HIP_TRY(hipEventRecord(plan->done, stream));

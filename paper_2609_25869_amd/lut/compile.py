@@ -109,7 +109,8 @@ def artifact(table, schema, catalog, provenance: Dict) -> Dict:
         "format": "bsa-plan-table",
         "version": 1,
         "arch": "gfx950",
-        "catalog": [[e["id"], e["tq"], e["tkv"], e["split"], e["stages"], e["waves"]] for e in catalog],
+        "catalog": [[e["id"], e["tq"], e["tkv"], e["split"], e["stages"], e["waves"], e["xcd_group"]]
+                    for e in catalog],
         "schema": [[n, list(e)] for n, e in schema],
         "regimes": regimes,
         "provenance": provenance,
@@ -162,7 +163,8 @@ def artifact_v2(regions, catalog, provenance: Dict) -> Dict:
         "format": "bsa-plan-table",
         "version": 2,
         "arch": "gfx950",
-        "catalog": [[e["id"], e["tq"], e["tkv"], e["split"], e["stages"], e["waves"]] for e in catalog],
+        "catalog": [[e["id"], e["tq"], e["tkv"], e["split"], e["stages"], e["waves"], e["xcd_group"]]
+                    for e in catalog],
         "features": list(tree.FEATURES),
         "regimes": regimes,
         "partition": {"%d:%d" % key[:2]: {"kind": regions[key]["kind"], "depth": regions[key]["depth"],

@@ -53,7 +53,7 @@ def test_binding_covers_every_entry_point():
 
 
 def test_version_and_status_strings():
-    assert bsa.version() == (1, 0)
+    assert bsa.version() == (1, 1)
     lib = bsa._lib
     for s in range(6):
         assert lib.bsa_status_string(s)
@@ -61,15 +61,28 @@ def test_version_and_status_strings():
 
 
 def test_catalog_layout():
+    """Every catalog entry names the kernel that runs it: wavefronts and ring
+    depth as launched (one wave per 32 query rows and 64 KB rings, except
+    T = (256, 32), four waves of 64 rows with an eight-slot ring); ids 24-29
+    repeat the split-free tiles with the all-XCD traversal order."""
     cat = bsa.catalog()
-    assert len(cat) == 24
+    assert len(cat) == 30
     tqs, tkvs, splits = (64, 128, 256), (32, 64), (1, 2, 4, 8)
-    for e in cat:
+
+    def launched(tq, tkv):
+        return (8, 4) if (tq, tkv) == (256, 32) else ((4 if tkv == 32 else 2), tq // 32)
+
+    for e in cat[:24]:
         i = e["id"]
         assert (e["tq"], e["tkv"], e["split"]) == (tqs[i // 8], tkvs[(i // 4) % 2], splits[i % 4])
-        assert e["waves"] == e["tq"] // 32
-        assert e["stages"] == (4 if e["tkv"] == 32 else 2)
-    st = bsa._lib.bsa_catalog_get(24, ctypes.byref(_ffi.CatalogEntry()))
+        assert (e["stages"], e["waves"]) == launched(e["tq"], e["tkv"])
+        assert e["xcd_group"] == 2
+    for j, e in enumerate(cat[24:30]):
+        assert (e["id"], e["tq"], e["tkv"], e["split"], e["xcd_group"]) == (24 + j, tqs[j // 2], tkvs[j % 2], 1, 8)
+        assert (e["stages"], e["waves"]) == launched(e["tq"], e["tkv"])
+    # the (256, 32) plans run four 64-row waves through an eight-slot ring
+    assert [(e["stages"], e["waves"]) for e in cat[16:20]] == [(8, 4)] * 4
+    st = bsa._lib.bsa_catalog_get(30, ctypes.byref(_ffi.CatalogEntry()))
     assert st == _ffi.BSA_ERR_INVALID
 
 
@@ -114,7 +127,8 @@ ARCH_OK = "gfx950"
 def artifact(table, schema=SCHEMA, **over):
     doc = {
         "format": "bsa-plan-table", "version": 1, "arch": ARCH_OK,
-        "catalog": [[e["id"], e["tq"], e["tkv"], e["split"], e["stages"], e["waves"]] for e in bsa.catalog()],
+        "catalog": [[e["id"], e["tq"], e["tkv"], e["split"], e["stages"], e["waves"], e["xcd_group"]]
+                    for e in bsa.catalog()],
         "schema": [[n, list(e)] for n, e in schema],
         "regimes": [{"key": list(k), "bucket": list(b), "ranking": list(r)}
                     for k, bt in table.items() for b, r in bt.items()],
