@@ -1,4 +1,4 @@
-"""Plan-selection ablation on complete requests (Section 6, A0 / A1 / A2).
+"""Plan-selection ablation on complete requests (Section 7.4, A0 / A1 / A2).
 
   A0  Direct: the key's base plan (physical tile = logical block when the
       catalog has it), prepared on every pass.
@@ -15,7 +15,7 @@ already on the device.  Pass 1 is the cold unique request, passes 2-4 the
 warm exact repeats, and the amortized latency averages all four.  The
 kernel columns are the execution time of the plan each variant ends with.
 
-Dispatch overhead (the measurement of Table 7, Section 6): per case, the
+Dispatch overhead (the measurement of Table 6, Section 7.4): per case, the
 wall time of A2's preparation alone (bsa_plan: the mask state on the device,
 the one statistics copy, lookup and eligibility, the metadata launches;
 stream synchronised), PASSES times, and of the host lookup and eligibility
@@ -162,7 +162,7 @@ def run_case(torch, bsa, case):
 
 
 def summarize(records):
-    """Paired-case geometric means of the latency ratios (Table 8 layout)."""
+    """Paired-case geometric means of the latency ratios (Table 7 layout)."""
     def gm(xs):
         xs = [x for x in xs if x > 0 and x == x]
         return math.exp(sum(math.log(x) for x in xs) / len(xs)) if xs else float("nan")

@@ -207,7 +207,7 @@ def _regret_summary(regrets, misses, per_key):
 
 
 def kernel_ablations(pick, base_plan, catalog, records) -> Dict:
-    """Kernel-time ablations from profiling records (Section 6).
+    """Kernel-time ablations from profiling records (organization: Section 7.3, Table 5; selection: Section 7.4).
 
     A0 / A1 / A2: the key's base (Direct) plan, the fastest measured eligible
     plan (what an exhaustive search finds), and the table's pick
@@ -352,7 +352,7 @@ def write_report(path: str, table, base, catalog, prof_recs, eval_recs, candidat
         rows = [("all keys", ablation.dispatch_summary(recs)),
                 ("64:64", ablation.dispatch_summary(recs, (64, 64)))]
         if rows[0][1]["cases"]:
-            lines += ["## Dispatch overhead per request (the measurement of Table 7)", "",
+            lines += ["## Dispatch overhead per request (the measurement of Table 6)", "",
                       "`bsa_plan` is the whole request-path preprocessing: the mask state on the device, the one "
                       "statistics copy and synchronisation, lookup and eligibility on the host, and the metadata "
                       "launches of the selected plan (wall time, stream synchronised). The lookup and "
