@@ -220,9 +220,16 @@ struct bsa_plan_s {
     if (done) (void)hipEventDestroy(done);
   }
 
+  // Fault injection for tests: BSA_FAULT_ALLOC=n makes the n-th device
+  // allocation of a plan fail (n >= 1), so that error paths that already
+  // hold allocations can be checked for leaks.
   bsa_status alloc(void** p, size_t bytes) {
     *p = nullptr;
-    if (std::getenv("BSA_FAULT_ALLOC")) return fail(BSA_ERR_OOM, "device allocation failed (injected by BSA_FAULT_ALLOC)");
+    if (const char* f = std::getenv("BSA_FAULT_ALLOC")) {
+      const long n = std::atol(f);
+      if (n >= 1 && (long)allocs.size() + 1 == n)
+        return fail(BSA_ERR_OOM, "device allocation " + std::to_string(n) + " failed (injected by BSA_FAULT_ALLOC)");
+    }
     if (bytes == 0) bytes = 256;
     hipError_t e = hipMallocAsync(p, bytes, stream);
     if (e != hipSuccess) {
