@@ -130,12 +130,16 @@ typedef struct {
                         of tasks (the same heads), 2 spreads four stretches over the chip */
 } bsa_catalog_entry;
 
-/* Regime-lookup input z_A(R) = <k_A(R), u_A(R), s_A(M)> (Eq. 3). */
+/* Regime-lookup input z_A(R) = <k_A(R), u_A(R), s_A(M)> (Eq. 3).  Tables
+ * may also use two features derived from these: query_rows = batch_heads *
+ * ceil(seq_q / bq), and row_imbalance = max_row_nnz * query_rows / nnz (the
+ * longest query-block row against the mean row). */
 typedef struct {
   int32_t bq, bkv, dtype, head_dim; /* request key (with the library's architecture) */
   int64_t batch_heads;              /* batch x heads of the segment */
   int64_t seq_q, seq_kv;
   int64_t nnz, blocks, run_blocks;  /* mask statistics */
+  int64_t max_row_nnz;              /* largest active-block count of one query-block row */
 } bsa_regime_query;
 
 /* Export selectors for bsa_plan_export. */

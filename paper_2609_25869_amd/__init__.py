@@ -119,10 +119,11 @@ class Lut:
 
 
 def regime_query(bq: int, bkv: int, batch_heads: int, seq_q: int, seq_kv: int, nnz: int, blocks: int,
-                 run_blocks: int, head_dim: int = 128, dtype: int = DTYPE_BF16) -> RegimeQuery:
+                 run_blocks: int, head_dim: int = 128, dtype: int = DTYPE_BF16, max_row_nnz: int = 0) -> RegimeQuery:
     z = RegimeQuery()
     z.bq, z.bkv, z.dtype, z.head_dim = bq, bkv, dtype, head_dim
     z.batch_heads, z.seq_q, z.seq_kv, z.nnz, z.blocks, z.run_blocks = batch_heads, seq_q, seq_kv, nnz, blocks, run_blocks
+    z.max_row_nnz = max_row_nnz
     return z
 
 

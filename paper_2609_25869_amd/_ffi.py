@@ -52,7 +52,7 @@ class CatalogEntry(ctypes.Structure):
 class RegimeQuery(ctypes.Structure):
     _fields_ = [("bq", c_i32), ("bkv", c_i32), ("dtype", c_i32), ("head_dim", c_i32),
                 ("batch_heads", c_i64), ("seq_q", c_i64), ("seq_kv", c_i64),
-                ("nnz", c_i64), ("blocks", c_i64), ("run_blocks", c_i64)]
+                ("nnz", c_i64), ("blocks", c_i64), ("run_blocks", c_i64), ("max_row_nnz", c_i64)]
 
 
 # (name, restype, argtypes) of every exported entry point

@@ -221,8 +221,8 @@ bool as_int_list(const JVal* v, std::vector<int64_t>* out) {
   return true;
 }
 
-const char* kRatioFeatures[] = {"density", "run_coverage"};
-const char* kIntFeatures[] = {"seq_q", "seq_kv", "batch_heads"};
+const char* kRatioFeatures[] = {"density", "run_coverage", "row_imbalance"};
+const char* kIntFeatures[] = {"seq_q", "seq_kv", "batch_heads", "query_rows"};
 
 bool known_feature(const std::string& n) {
   for (const char* f : kRatioFeatures)
@@ -362,20 +362,53 @@ bool lut_parse(const std::string& text, Lut* out, std::string* err) {
   return true;
 }
 
+namespace {
+
+// Integer feature `n` of z.  query_rows is the number of logical query-block
+// rows, batch x heads x ceil(seq_q / B_Q).
+int64_t int_feature(const std::string& n, const bsa_regime_query& z) {
+  if (n == "seq_q") return z.seq_q;
+  if (n == "seq_kv") return z.seq_kv;
+  if (n == "query_rows") return z.bq > 0 ? z.batch_heads * ((z.seq_q + z.bq - 1) / z.bq) : 0;
+  return z.batch_heads;
+}
+
+bool is_ratio(const std::string& n) { return n == "density" || n == "run_coverage" || n == "row_imbalance"; }
+
+// Ratio feature `n` of z as (numerator, denominator); a zero denominator
+// reads as 0.  row_imbalance = max_row_nnz * query_rows / nnz.
+void ratio_feature(const std::string& n, const bsa_regime_query& z, __int128* num, __int128* den) {
+  if (n == "density") {
+    *num = z.nnz;
+    *den = z.blocks;
+  } else if (n == "run_coverage") {
+    *num = z.run_blocks;
+    *den = z.nnz;
+  } else {
+    *num = (__int128)z.max_row_nnz * int_feature("query_rows", z);
+    *den = z.nnz;
+  }
+  if (*den <= 0) {
+    *num = 0;
+    *den = 1;
+  }
+}
+
+}  // namespace
+
 std::vector<int64_t> lut_bucket(const Lut& lut, const bsa_regime_query& z) {
   std::vector<int64_t> b;
   for (size_t f = 0; f < lut.feature_names.size(); ++f) {
     const std::string& n = lut.feature_names[f];
     const auto& edges = lut.feature_edges[f];
     int64_t idx = 0;
-    if (n == "density" || n == "run_coverage") {
-      int64_t num = n == "density" ? z.nnz : z.run_blocks;
-      int64_t den = n == "density" ? z.blocks : z.nnz;
-      if (den <= 0) { num = 0; den = 1; }
+    if (is_ratio(n)) {
+      __int128 num, den;
+      ratio_feature(n, z, &num, &den);
       for (int64_t e : edges)
-        if ((__int128)num * 10000 >= (__int128)e * den) ++idx;
+        if (num * 10000 >= (__int128)e * den) ++idx;
     } else {
-      const int64_t v = n == "seq_q" ? z.seq_q : n == "seq_kv" ? z.seq_kv : z.batch_heads;
+      const int64_t v = int_feature(n, z);
       for (int64_t e : edges)
         if (v >= e) ++idx;
     }
@@ -388,14 +421,12 @@ namespace {
 
 // feature `n` of z >= edge (ratio features exactly, edges in units of 1e-4)
 bool feature_ge(const std::string& n, const bsa_regime_query& z, int64_t edge) {
-  if (n == "density" || n == "run_coverage") {
-    int64_t num = n == "density" ? z.nnz : z.run_blocks;
-    int64_t den = n == "density" ? z.blocks : z.nnz;
-    if (den <= 0) { num = 0; den = 1; }
-    return (__int128)num * 10000 >= (__int128)edge * den;
+  if (is_ratio(n)) {
+    __int128 num, den;
+    ratio_feature(n, z, &num, &den);
+    return num * 10000 >= (__int128)edge * den;
   }
-  const int64_t v = n == "seq_q" ? z.seq_q : n == "seq_kv" ? z.seq_kv : z.batch_heads;
-  return v >= edge;
+  return int_feature(n, z) >= edge;
 }
 
 }  // namespace

@@ -279,6 +279,7 @@ bsa_status select_segment_plan(Segment& sg, const bsa_shapes& s, const bsa_plan_
   z.nnz = sg.nnz;
   z.blocks = sg.blocks;
   z.run_blocks = sg.run_blocks;
+  z.max_row_nnz = sg.max_row_nnz;
   bool hit = false;
   std::vector<int32_t> ranking;
   if (opts.select_mode == 1) {

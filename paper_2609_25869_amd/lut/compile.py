@@ -27,13 +27,24 @@ from typing import Dict, List, Sequence, Tuple
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 
-# Feature schema of the gfx950 table: predefined bucket edges.
-# seq_q in tokens, batch_heads in (batch x heads), ratios in units of 1e-4.
-# The sequence-length and head-count edges separate the short, few-head
-# requests of the wide corpus (Split-K and small tiles win there); on the
-# held-out splits this grid had the lowest selector regret of the grids and
-# decision-tree tables compared (gfx950_report.md).
+# Feature schema of the gfx950 table: predefined bucket edges.  query_rows
+# is batch x heads x ceil(seq_q / B_Q), the number of logical query-block
+# rows of the request (u_A of Eq. 3 folded into one count: how many
+# query-tile tasks there are to spread over 256 CUs, which decides whether
+# Split-K and small tiles pay); row_imbalance = max_row_nnz * query_rows /
+# nnz, the longest row against the mean row (near 1 for top-k and window
+# masks, well above 1 when heads differ in density); ratios in units of
+# 1e-4.  Chosen among candidate grids by source-grouped 4-fold
+# cross-validation on the training records (gfx950_report.md lists the
+# candidates with their held-out regret).
 SCHEMA: List[Tuple[str, List[int]]] = [
+    ("query_rows", [1024, 4096]),
+    ("density", [700, 2000]),
+    ("run_coverage", [9000]),
+    ("row_imbalance", [30000]),
+]
+# The grid of the previous table, kept for the report's comparison.
+SEQ_HEADS_SCHEMA: List[Tuple[str, List[int]]] = [
     ("seq_q", [6144, 24576, 98304]),
     ("batch_heads", [3, 12]),
     ("density", [700, 2000]),
@@ -41,8 +52,22 @@ SCHEMA: List[Tuple[str, List[int]]] = [
 ]
 
 # Profiling records the shipped table is built from, and held-out records.
-PROFILES = [os.path.join(HERE, "gfx950_profile.jsonl"), os.path.join(HERE, "gfx950_wide.jsonl")]
-EVALS = [os.path.join(HERE, "gfx950_eval.jsonl"), os.path.join(HERE, "gfx950_wide_eval.jsonl")]
+PROFILES = [os.path.join(HERE, "gfx950_profile.jsonl"), os.path.join(HERE, "gfx950_wide.jsonl"),
+            os.path.join(HERE, "gfx950_mixture.jsonl")]
+EVALS = [os.path.join(HERE, "gfx950_eval.jsonl"), os.path.join(HERE, "gfx950_wide_eval.jsonl"),
+         os.path.join(HERE, "gfx950_mixture_eval.jsonl")]
+
+
+def with_query_rows(rec: Dict) -> Dict:
+    """Add the derived features: query_rows = batch_heads * ceil(seq_q / B_Q)
+    and, when max_row_nnz is recorded, the numerator of row_imbalance =
+    max_row_nnz * query_rows / nnz."""
+    f = rec.get("features")
+    if f and "query_rows" not in f and "key" in rec:
+        f["query_rows"] = int(f["batch_heads"]) * (-(-int(f["seq_q"]) // int(rec["key"][0])))
+    if f and "max_row_nnz" in f and "imbalance_num" not in f:
+        f["imbalance_num"] = int(f["max_row_nnz"]) * int(f["query_rows"])
+    return rec
 
 
 def load_records(path) -> List[Dict]:
@@ -50,7 +75,7 @@ def load_records(path) -> List[Dict]:
     if not isinstance(path, str):
         return [r for p in path for r in load_records(p)]
     with open(path) as f:
-        return [json.loads(line) for line in f if line.strip()]
+        return [with_query_rows(json.loads(line)) for line in f if line.strip()]
 
 
 def feature_value(feats: Dict, name: str):
@@ -58,6 +83,8 @@ def feature_value(feats: Dict, name: str):
         return feats["nnz"], feats["blocks"]
     if name == "run_coverage":
         return feats["run_blocks"], feats["nnz"]
+    if name == "row_imbalance":
+        return feats["imbalance_num"], feats["nnz"]
     return feats[name]
 
 
@@ -73,6 +100,55 @@ def bucket(feats: Dict, schema: Sequence[Tuple[str, Sequence[int]]]) -> Tuple[in
         else:
             out.append(sum(1 for e in edges if v >= e))
     return tuple(out)
+
+
+def source_of(rec: Dict) -> Tuple:
+    """Mask source of a profiling case: generator family and density (the
+    stand-in for the model a mask came from).  A mixture request composes
+    its heads from several families and densities, so each one is a source
+    of its own (the stand-in for one model's mix of heads)."""
+    if rec.get("family") == "mixture":
+        return ("mixture", rec.get("id"))
+    return (rec.get("family"), rec.get("rho"))
+
+
+def cv_regret(records: Sequence[Dict], schema, base_plan, folds: int = 4) -> float:
+    """Geometric-mean selector regret of a grid schema under source-grouped
+    cross-validation on the training records: each fold's table is built
+    without the fold's sources and scored on them."""
+    sources = sorted({source_of(r) for r in records}, key=repr)
+    fold_of = {s: i % folds for i, s in enumerate(sources)}
+    total, n = 0.0, 0
+    for f in range(folds):
+        train = [r for r in records if fold_of[source_of(r)] != f]
+        test = [r for r in records if fold_of[source_of(r)] == f]
+        if not train or not test:
+            continue
+        a = regret_report(compile_table(train, schema, base_plan), schema, base_plan, test)["all"]
+        total += math.log(a["gm"]) * a["cases"]
+        n += a["cases"]
+    return math.exp(total / n) if n else float("nan")
+
+
+# Candidate grids the shipped schema was chosen from (lowest cross-validated
+# regret on the training records).
+CANDIDATE_SCHEMAS: List[List[Tuple[str, List[int]]]] = [
+    SCHEMA,
+    [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [9000]), ("row_imbalance", [25000])],
+    [("query_rows", [512, 2048, 8192]), ("density", [700, 2000]), ("run_coverage", [9000]),
+     ("row_imbalance", [30000])],
+    [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [5000, 9000])],
+    [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [9000])],
+    [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [8000])],
+    [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [5000])],
+    [("query_rows", [512, 2048, 8192]), ("density", [700, 2000]), ("run_coverage", [8000])],
+    [("query_rows", [512, 2048, 8192]), ("density", [700, 2000]), ("run_coverage", [5000])],
+    [("query_rows", [256, 1024, 4096, 16384]), ("density", [700, 2000]), ("run_coverage", [5000])],
+    [("query_rows", [1024, 4096]), ("density", [500, 1500, 3000]), ("run_coverage", [8000])],
+    [("query_rows", [1024, 4096]), ("seq_q", [24576]), ("density", [700, 2000]), ("run_coverage", [5000])],
+    SEQ_HEADS_SCHEMA,
+    [("seq_q", [32768, 98304]), ("batch_heads", [12]), ("density", [700, 2000]), ("run_coverage", [5000])],
+]
 
 
 def compile_table(records: Sequence[Dict], schema, base_plan) -> Dict[Tuple[int, ...], Dict[Tuple[int, ...], List[int]]]:
@@ -315,13 +391,14 @@ def write_report(path: str, table, base, catalog, prof_recs, eval_recs, candidat
                 "%g-%g" % (lo, hi) if hi != float("inf") else ">= %g" % lo, a["cases"], a["gm"], a["p95"],
                 100 * a["within_3pct"]))
     if candidates:
-        lines += ["", "## Regime partitions compared on the held-out cases (Section 5.1: predefined intervals or "
-                  "decision-tree thresholds)", "",
-                  "| partition (built from the profiling records) | GM | P95 | P99 | within 3% |",
-                  "|---|---:|---:|---:|---:|"]
-        for name, a in candidates:
-            lines.append("| %s | %.4f | %.4f | %.4f | %.1f%% |" % (name, a["gm"], a["p95"], a["p99"],
-                                                                 100 * a["within_3pct"]))
+        lines += ["", "## Regime partitions (Section 5.1: predefined intervals or decision-tree thresholds)", "",
+                  "The shipped grid is the candidate with the lowest source-grouped 4-fold cross-validated regret "
+                  "on the training records (CV GM); the held-out columns are reported, not used for the choice.",
+                  "", "| partition (built from the profiling records) | CV GM | held-out GM | P95 | P99 | within 3% |",
+                  "|---|---:|---:|---:|---:|---:|"]
+        for name, cv, a in candidates:
+            lines.append("| %s | %s | %.4f | %.4f | %.4f | %.1f%% |" % (
+                name, "%.4f" % cv if cv is not None else "-", a["gm"], a["p95"], a["p99"], 100 * a["within_3pct"]))
     lines += ["", "Held-out regret per request key (B_Q:B_KV):", "",
               "| key | cases | GM | P95 | max |", "|---|---:|---:|---:|---:|"]
     for k, a in regret_report(table, SCHEMA, base, eval_recs)["per_key"].items():
@@ -452,15 +529,15 @@ def main():
         if args.report:
             from . import tree
             ev = load_records(args.eval)
-            prev = [("seq_q", [32768, 98304]), ("batch_heads", [12]), ("density", [700, 2000]),
-                    ("run_coverage", [5000])]
-            cands = [("predefined intervals, shipped schema %s" % SCHEMA, regret_report(table, SCHEMA, base, ev)["all"]),
-                     ("predefined intervals, earlier schema %s" % prev,
-                      regret_report(compile_table(recs, prev, base), prev, base, ev)["all"]),
-                     ("decision trees per key (>= %d cases per leaf, depth by grouped CV)" % tree.MIN_LEAF,
-                      regret_report_v2(tree.compile_regions(recs, base), base, ev)["all"]),
-                     ("per key, tree or shipped intervals by grouped CV",
-                      regret_report_v2(tree.compile_regions(recs, base, grid_schema=SCHEMA), base, ev)["all"])]
+            cands = []
+            for sch in CANDIDATE_SCHEMAS:
+                cands.append(("predefined intervals %s%s" % (sch, " (shipped)" if sch is SCHEMA else ""),
+                              cv_regret(recs, sch, base),
+                              regret_report(compile_table(recs, sch, base), sch, base, ev)["all"]))
+            cands += [("decision trees per key (>= %d cases per leaf, depth by grouped CV)" % tree.MIN_LEAF, None,
+                       regret_report_v2(tree.compile_regions(recs, base), base, ev)["all"]),
+                      ("per key, tree or shipped intervals by grouped CV", None,
+                       regret_report_v2(tree.compile_regions(recs, base, grid_schema=SCHEMA), base, ev)["all"])]
             write_report(os.path.join(HERE, "gfx950_report.md"), table, base, bsa.catalog(), recs, ev, cands)
 
 

@@ -39,7 +39,7 @@ SEQ_LENS = [16384, 65536, 115200]
 BATCH_HEADS = [4, 24]
 FAMILIES = [("window", 0.05), ("window", 0.15), ("bernoulli", 0.03), ("bernoulli", 0.10), ("bernoulli", 0.30),
             ("topk", 0.12)]
-SPLIT_SEED = {"profile": 0, "eval": 1, "wide": 2, "wide_eval": 3}
+SPLIT_SEED = {"profile": 0, "eval": 1, "wide": 2, "wide_eval": 3, "mixture": 4, "mixture_eval": 5}
 FRAMES = 16
 
 # The wide splits draw, per request key, random combinations of a larger
@@ -51,6 +51,16 @@ WIDE_SOURCES = [("window", 0.03), ("window", 0.08), ("window", 0.15), ("window",
                 ("bernoulli", 0.40), ("topk", 0.06), ("topk", 0.12), ("topk", 0.25)]
 WIDE_PER_KEY = {"wide": 96, "wide_eval": 48}
 
+# The mixture splits: requests whose heads draw their masks from different
+# families (window 40%, top-k 40%, Bernoulli 20%) at densities from
+# {2, 5, 10, 25, 50}%, per head, as in a model whose heads attend
+# differently; long sequences and many heads.
+MIX_SEQ = [16384, 32768, 65536, 115200, 131072]
+MIX_BH = [8, 24, 48]
+MIX_PER_KEY = {"mixture": 12, "mixture_eval": 6}
+MIX_FAMILIES = [("window", 0.4), ("topk", 0.4), ("bernoulli", 0.2)]
+MIX_RHO = [0.02, 0.05, 0.10, 0.25, 0.50]
+
 
 def log(msg):
     print("[profile] " + msg, flush=True)
@@ -59,6 +69,14 @@ def log(msg):
 def corpus(split):
     """The deterministic case list of one split."""
     cases = []
+    if split in MIX_PER_KEY:
+        import random
+        rng = random.Random(1000 + SPLIT_SEED[split])
+        for geom in GEOMETRIES:
+            for _ in range(MIX_PER_KEY[split]):
+                cases.append(dict(id="%s-%d" % (split, len(cases)), geometry=list(geom), N=rng.choice(MIX_SEQ),
+                                  bh=rng.choice(MIX_BH), family="mixture", rho=0.0, seed=rng.randrange(1 << 30)))
+        return cases
     if split in WIDE_PER_KEY:
         import random
         rng = random.Random(1000 + SPLIT_SEED[split])
@@ -91,6 +109,20 @@ def make_mask(torch, case, q, k):
     diag = (torch.arange(nqb, device=dev)[:, None] * bq < (torch.arange(nkb, device=dev)[None, :] + 1) * bkv) & \
            (torch.arange(nkb, device=dev)[None, :] * bkv < (torch.arange(nqb, device=dev)[:, None] + 1) * bq)
     out = torch.empty((bh, nqb, nkb), dtype=torch.uint8, device=dev)
+    if case["family"] == "mixture":
+        import random
+        pick = random.Random(case["seed"])
+        for h in range(bh):
+            u, acc, fam = pick.random(), 0.0, MIX_FAMILIES[-1][0]
+            for name, w in MIX_FAMILIES:
+                acc += w
+                if u < acc:
+                    fam = name
+                    break
+            rho = pick.choice(MIX_RHO)
+            one = dict(case, family=fam, rho=rho, bh=1, seed=pick.randrange(1 << 30))
+            out[h] = make_mask(torch, one, q[:, :, h:h + 1, :], k[:, :, h:h + 1, :])[0]
+        return out
     if case["family"] == "window":
         # tokens as FRAMES frames of N/FRAMES positions; active when the block
         # centres are within one frame and within a spatial half-width w
@@ -197,7 +229,7 @@ def profile_case(torch, bsa, case, reps=3):
         if feats is None:
             info = p.info(0)
             feats = {"seq_q": N, "seq_kv": N, "batch_heads": bh, "nnz": info["nnz"], "blocks": info["blocks"],
-                     "run_blocks": info["run_blocks"]}
+                     "run_blocks": info["run_blocks"], "max_row_nnz": info["max_row_nnz"]}
         t = kernel_time(torch, stream, lambda: bsa.forward(p, q, k, v, o, None, stream=stream), reps)
         p.destroy()
         ok = bool(torch.isfinite(o).all().item())
@@ -212,13 +244,61 @@ def profile_case(torch, bsa, case, reps=3):
             "features": feats, "latency_ms": {str(p): t for p, t in lat.items()}, "invalid": invalid}
 
 
+def case_features(torch, bsa, case):
+    """The regime features of a case alone (mask statistics from bsa_plan
+    with the base plan), without timing any plan."""
+    bq, bkv = case["geometry"]
+    N, bh = case["N"], case["bh"]
+    dev = torch.device("cuda")
+    g = torch.Generator(device=dev)
+    g.manual_seed(case["seed"] + 7)
+    q = torch.randn((1, N, bh, 128), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    k = torch.randn((1, N, bh, 128), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    mask = make_mask(torch, case, q, k)
+    nqb, nkb = mask.shape[1], mask.shape[2]
+    p = bsa.plan(mask, bq, bkv, bsa.shapes_of(q, k, k, q), head_offset=[h * nqb * nkb for h in range(bh)],
+                 stride_b=0, force_plan=bsa.base_plan(bq, bkv))
+    info = p.info(0)
+    p.destroy()
+    return {"seq_q": N, "seq_kv": N, "batch_heads": bh, "nnz": info["nnz"], "blocks": info["blocks"],
+            "run_blocks": info["run_blocks"], "max_row_nnz": info["max_row_nnz"]}
+
+
+def refeature(args):
+    """Add max_row_nnz to the records of a split profiled before it was
+    recorded: the masks are regenerated from the case seeds, and the other
+    statistics must come out as recorded."""
+    import torch
+    import paper_2609_25869_amd as bsa
+    by_id = {c["id"]: c for c in corpus(args.split)}
+    recs = [json.loads(l) for l in open(args.out) if l.strip()]
+    t0 = time.time()
+    for r in recs:
+        if "max_row_nnz" in (r["features"] or {}):
+            continue
+        f = case_features(torch, bsa, by_id[r["id"]])
+        old = r["features"]
+        assert all(f[k] == old[k] for k in old), (r["id"], old, f)
+        r["features"] = f
+    with open(args.out + ".tmp", "w") as fo:
+        for r in recs:
+            fo.write(json.dumps(r) + "\n")
+    os.replace(args.out + ".tmp", args.out)
+    log("refeatured %d records of %s in %.1f s" % (len(recs), args.split, time.time() - t0))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", required=True)
     ap.add_argument("--split", default="profile", choices=sorted(SPLIT_SEED))
     ap.add_argument("--budget", type=float, default=600.0, help="stop starting new cases after this many seconds")
     ap.add_argument("--only", default="", help="comma-separated geometries 'bq:bkv' to profile")
+    ap.add_argument("--refeature", action="store_true",
+                    help="only add the max_row_nnz statistic to the existing records in --out (no timing)")
     args = ap.parse_args()
+    if args.refeature:
+        refeature(args)
+        return
     import torch
     import paper_2609_25869_amd as bsa
 

@@ -33,8 +33,8 @@ from typing import Callable, Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
-FEATURES = ["seq_q", "batch_heads", "density", "run_coverage"]
-RATIOS = {"density": ("nnz", "blocks"), "run_coverage": ("run_blocks", "nnz")}
+FEATURES = ["seq_q", "batch_heads", "density", "run_coverage", "query_rows", "row_imbalance"]
+RATIOS = {"density": ("nnz", "blocks"), "run_coverage": ("run_blocks", "nnz"), "row_imbalance": ("imbalance_num", "nnz")}
 MIN_LEAF = 32
 DEPTHS = (0, 1, 2, 3, 4)
 
@@ -170,6 +170,9 @@ def grow(cases: Sequence[Dict], depth: int, min_leaf: int = MIN_LEAF) -> List[Tu
 
 
 def source_of(case: Dict) -> Tuple:
+    """Generator family and density; each mixture request is its own source."""
+    if case.get("family") == "mixture":
+        return ("mixture", case.get("id"))
     return (case.get("family"), case.get("rho"))
 
 

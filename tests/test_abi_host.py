@@ -267,3 +267,57 @@ def test_null_arguments_are_rejected():
     assert lib.bsa_forward(None, None, None, None, None, None, None) == _ffi.BSA_ERR_INVALID
     assert lib.bsa_plan_destroy(None) == _ffi.BSA_OK
     assert lib.bsa_last_error()
+
+
+def test_query_rows_feature_is_counted_from_its_definition(tmp_path):
+    """The derived feature query_rows = batch x heads x ceil(seq_q / B_Q) (the
+    number of logical query-block rows) is computed by the library from the
+    regime query, so a grid over it buckets like the oracle's restatement."""
+    schema = [("query_rows", [1024, 4096]), ("density", [500, 2000])]
+    rng = np.random.default_rng(3)
+    table = {}
+    for key in [(64, 64, 0, 128), (128, 32, 0, 128), (16, 16, 0, 128)]:
+        for b0 in range(3):
+            for b1 in range(3):
+                table.setdefault(key, {})[(b0, b1)] = [int(x) for x in rng.choice(24, 3, replace=False)]
+    doc = artifact(table, schema)
+    lut = bsa.Lut(write(tmp_path, doc))
+    for t in range(300):
+        bq, bkv = [(64, 64), (128, 32), (16, 16)][t % 3]
+        seq_q = int(rng.choice([1, 1000, 1024, 4095, 4096, 65536, 131071]))
+        bh = int(rng.choice([1, 2, 8, 24, 48]))
+        # half the probes sit exactly on an edge of the row count
+        if t % 2:
+            bh = 1
+            seq_q = bq * int(rng.choice([1023, 1024, 4095, 4096]))
+        blocks = int(rng.integers(1, 5000))
+        nnz = int(rng.integers(0, blocks + 1))
+        z = bsa.regime_query(bq, bkv, bh, seq_q, seq_q, nnz=nnz, blocks=blocks, run_blocks=0)
+        feats = {"query_rows": bh * -(-seq_q // bq), "density": (nnz, blocks)}
+        want = table[(bq, bkv, 0, 128)][regime.bucket_of(feats, schema)]
+        assert bsa.lut_rank(z, lut) == (want, 1), (bq, seq_q, bh)
+    lut.close()
+
+
+def test_row_imbalance_feature_is_counted_from_its_definition(tmp_path):
+    """row_imbalance = max_row_nnz * query_rows / nnz, compared with its
+    edges exactly as integers like the other ratios (0 when nnz is 0)."""
+    schema = [("row_imbalance", [15000, 30000])]
+    table = {(64, 64, 0, 128): {(0,): [0], (1,): [8], (2,): [16]}}
+    lut = bsa.Lut(write(tmp_path, artifact(table, schema)))
+    rng = np.random.default_rng(4)
+    cases = [(0, 0, 7, 0), (1, 100, 150, 1), (1, 100, 151, 1), (2, 1000, 3000, 64)]
+    for _ in range(200):
+        cases.append((int(rng.integers(1, 5)), int(rng.integers(0, 5000)), int(rng.integers(0, 3000)),
+                      int(rng.integers(64, 20000))))
+    for bh, nnz, max_row, seq_q in cases:
+        rows = bh * -(-seq_q // 64)
+        z = bsa.regime_query(64, 64, bh, seq_q, seq_q, nnz=nnz, blocks=max(1, nnz) * 4, run_blocks=0,
+                             max_row_nnz=max_row)
+        feats = {"row_imbalance": (max_row * rows, nnz)}
+        want = table[(64, 64, 0, 128)][regime.bucket_of(feats, schema)]
+        assert bsa.lut_rank(z, lut) == (want, 1), (bh, nnz, max_row, seq_q)
+    # exactly on an edge: one row of 3 blocks against a mean of 1 (3.0 = 30000 / 1e4)
+    z = bsa.regime_query(64, 64, 1, 64 * 4, 64 * 4, nnz=4, blocks=16, run_blocks=0, max_row_nnz=3)
+    assert bsa.lut_rank(z, lut) == ([16], 1)
+    lut.close()

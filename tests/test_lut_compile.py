@@ -31,22 +31,27 @@ def synthetic_records(seed, n=200):
         nnz = int(rng.integers(0, blocks + 1))
         feats = {"seq_q": int(rng.choice([4096, 65536, 131072])), "seq_kv": 4096,
                  "batch_heads": int(rng.choice([2, 48])), "nnz": nnz, "blocks": blocks,
-                 "run_blocks": int(rng.integers(0, nnz + 1))}
+                 "run_blocks": int(rng.integers(0, nnz + 1)), "max_row_nnz": int(rng.integers(0, 4 * nnz // 3 + 2))}
         lat = {str(p): float(rng.choice([0.5, 1.0, 1.25, 2.0])) for p in range(24) if rng.random() < 0.85}
-        recs.append({"id": "s%d" % i, "key": keys[i % 3], "features": feats, "latency_ms": lat})
+        recs.append(lutc.with_query_rows({"id": "s%d" % i, "key": keys[i % 3], "features": feats, "latency_ms": lat}))
     return recs
 
 
-def oracle_features(f):
-    return {"seq_q": f["seq_q"], "seq_kv": f["seq_kv"], "batch_heads": f["batch_heads"],
-            "density": (f["nnz"], f["blocks"]), "run_coverage": (f["run_blocks"], f["nnz"])}
+def oracle_features(f, key):
+    """The regime features of Eq. 3 from their definitions: query_rows is
+    batch x heads x ceil(seq_q / B_Q) logical query-block rows, and
+    row_imbalance is max_row_nnz * query_rows / nnz."""
+    rows = f["batch_heads"] * math.ceil(f["seq_q"] / key[0])
+    return {"seq_q": f["seq_q"], "seq_kv": f["seq_kv"], "batch_heads": f["batch_heads"], "query_rows": rows,
+            "density": (f["nnz"], f["blocks"]), "run_coverage": (f["run_blocks"], f["nnz"]),
+            "row_imbalance": (f["max_row_nnz"] * rows, f["nnz"])}
 
 
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_compile_matches_the_algorithm_restatement(seed):
     recs = synthetic_records(seed)
     got = lutc.compile_table(recs, lutc.SCHEMA, base)
-    cases = [{"id": r["id"], "key": tuple(r["key"]), "features": oracle_features(r["features"])} for r in recs]
+    cases = [{"id": r["id"], "key": tuple(r["key"]), "features": oracle_features(r["features"], r["key"])} for r in recs]
     lat = {(r["id"], int(p)): t for r in recs for p, t in r["latency_ms"].items()}
     want = regime.compile_table(cases, lat, lutc.SCHEMA, base)
     assert got == want
@@ -54,7 +59,7 @@ def test_compile_matches_the_algorithm_restatement(seed):
 
 def test_bucket_matches_the_algorithm_restatement():
     for r in synthetic_records(5, 300):
-        assert lutc.bucket(r["features"], lutc.SCHEMA) == regime.bucket_of(oracle_features(r["features"]), lutc.SCHEMA)
+        assert lutc.bucket(r["features"], lutc.SCHEMA) == regime.bucket_of(oracle_features(r["features"], r["key"]), lutc.SCHEMA)
 
 
 def test_shipped_artifact_is_the_compiled_profile():
@@ -71,8 +76,8 @@ def test_profile_covers_every_geometry_and_validated_every_plan():
     keys = {tuple(r["key"][:2]) for r in recs}
     assert {(128, 128), (128, 64), (64, 64), (64, 32), (32, 32), (32, 16), (16, 16), (128, 32), (32, 128)} <= keys
     for r in recs:
-        eligible = [p for p in range(24) if bsa.plan_eligible(p, r["key"][0], r["key"][1],
-                                                               bsa.make_shapes(1, 1, 1024, 1024))]
+        eligible = [e["id"] for e in bsa.catalog() if bsa.plan_eligible(e["id"], r["key"][0], r["key"][1],
+                                                                        bsa.make_shapes(1, 1, 1024, 1024))]
         assert sorted(int(p) for p in r["latency_ms"]) == eligible, r["id"]
         assert not r.get("invalid")
 
@@ -83,7 +88,8 @@ def test_library_uses_the_shipped_table_by_default():
     for r in lutc.load_records(EVAL)[::7]:
         f = r["features"]
         z = bsa.regime_query(r["key"][0], r["key"][1], f["batch_heads"], f["seq_q"], f["seq_kv"], f["nnz"],
-                             f["blocks"], f["run_blocks"])
+                             f["blocks"], f["run_blocks"],
+                             max_row_nnz=f["max_row_nnz"])
         ranking, hit = bsa.lut_rank(z)
         want = table.get(tuple(r["key"]), {}).get(lutc.bucket(f, lutc.SCHEMA))
         assert hit == (want is not None)

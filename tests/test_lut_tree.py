@@ -18,9 +18,13 @@ def base(key):
     return bsa.base_plan(key[0], key[1])
 
 
-def oracle_features(f):
+def oracle_features(f, bq=64):
+    """Regime features from their definitions (query_rows = batch x heads x
+    ceil(seq_q / B_Q), row_imbalance = max_row_nnz * query_rows / nnz)."""
+    rows = f["batch_heads"] * math.ceil(f["seq_q"] / bq)
     return {"seq_q": f["seq_q"], "batch_heads": f["batch_heads"], "density": (f["nnz"], f["blocks"]),
-            "run_coverage": (f["run_blocks"], f["nnz"])}
+            "run_coverage": (f["run_blocks"], f["nnz"]), "query_rows": rows,
+            "row_imbalance": (f["max_row_nnz"] * rows, f["nnz"])}
 
 
 def structured_records(seed, n=240, key=(64, 64, 0, 128)):
@@ -36,9 +40,10 @@ def structured_records(seed, n=240, key=(64, 64, 0, 128)):
                "8": 1.1, "0": 2.0 + rng.random()}
         lat = {p: t * (1 + 0.01 * rng.random()) for p, t in lat.items()}
         feats = {"seq_q": int(rng.choice([8192, 65536])), "seq_kv": 8192, "batch_heads": int(rng.choice([4, 24])),
-                 "nnz": nnz, "blocks": blocks, "run_blocks": int(rng.integers(0, nnz + 1))}
-        recs.append({"id": "t%d" % i, "key": list(key), "family": "f%d" % (i % 5), "rho": 0.1,
-                     "features": feats, "latency_ms": lat})
+                 "nnz": nnz, "blocks": blocks, "run_blocks": int(rng.integers(0, nnz + 1)),
+                 "max_row_nnz": int(rng.integers(0, nnz + 1))}
+        recs.append(lutc.with_query_rows({"id": "t%d" % i, "key": list(key), "family": "f%d" % (i % 5),
+                                          "rho": 0.1, "features": feats, "latency_ms": lat}))
     return recs
 
 
@@ -73,8 +78,10 @@ def test_regions_partition_every_case_and_random_query():
     for _ in range(300):
         blocks = int(rng.integers(1, 20000))
         nnz = int(rng.integers(0, blocks + 1))
-        probes.append({"seq_q": int(rng.integers(1, 200000)), "batch_heads": int(rng.integers(1, 64)),
-                       "nnz": nnz, "blocks": blocks, "run_blocks": int(rng.integers(0, nnz + 1))})
+        f = {"seq_q": int(rng.integers(1, 200000)), "batch_heads": int(rng.integers(1, 64)),
+             "nnz": nnz, "blocks": blocks, "run_blocks": int(rng.integers(0, nnz + 1)),
+             "max_row_nnz": int(rng.integers(0, nnz + 1))}
+        probes.append(lutc.with_query_rows({"key": [64, 64, 0, 128], "features": f})["features"])
     for f in probes:
         inside = [region for region, _, _ in leaves if tree.in_region(f, region)]
         assert len(inside) == 1
@@ -108,14 +115,15 @@ def test_library_lookup_matches_the_regions(tmp_path):
         nnz = edges[t % len(edges)] if (t % 4 == 1 and edges and edges[t % len(edges)] <= 10000) \
             else int(rng.integers(0, blocks + 1))
         z = bsa.regime_query(bq, bkv, int(rng.choice([4, 24])), int(rng.choice([8192, 65536])), 8192,
-                             nnz=nnz, blocks=blocks, run_blocks=int(rng.integers(0, nnz + 1)))
+                             nnz=nnz, blocks=blocks, run_blocks=int(rng.integers(0, nnz + 1)),
+                             max_row_nnz=int(rng.integers(0, nnz + 1)))
         feats = {"seq_q": z.seq_q, "batch_heads": z.batch_heads, "nnz": nnz, "blocks": blocks,
-                 "run_blocks": z.run_blocks}
+                 "run_blocks": z.run_blocks, "max_row_nnz": z.max_row_nnz}
         key = (bq, bkv, 0, 128)
         # Algorithm 2's lookup over the key's regions, by the oracle's leaf test
         leaves = [(region, ranking) for region, ranking, _ in regions.get(key, {}).get("regimes", [])]
-        want, hit = regime.lookup_regions(leaves, oracle_features(feats), tree.FEATURES, base(key))
-        assert sum(regime.region_contains(oracle_features(feats), r, tree.FEATURES) for r, _ in leaves) <= 1
+        want, hit = regime.lookup_regions(leaves, oracle_features(feats, bq), tree.FEATURES, base(key))
+        assert sum(regime.region_contains(oracle_features(feats, bq), r, tree.FEATURES) for r, _ in leaves) <= 1
         got, ghit = bsa.lut_rank(z, lut)
         assert (got, ghit) == (want, hit), (t, key, feats)
         assert tree.select(regions, key, feats, base(key)) == (want, hit)
