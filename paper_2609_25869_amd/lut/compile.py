@@ -31,13 +31,19 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 # is batch x heads x ceil(seq_q / B_Q), the number of logical query-block
 # rows of the request (u_A of Eq. 3 folded into one count: how many
 # query-tile tasks there are to spread over 256 CUs, which decides whether
-# Split-K and small tiles pay); row_imbalance = max_row_nnz * query_rows /
-# nnz, the longest row against the mean row (near 1 for top-k and window
-# masks, well above 1 when heads differ in density); ratios in units of
-# 1e-4.  Chosen among candidate grids by source-grouped 4-fold
-# cross-validation on the training records (gfx950_report.md lists the
-# candidates with their held-out regret).
+# Split-K and small tiles pay); ratios in units of 1e-4.  Chosen among
+# candidate grids by source-grouped 4-fold cross-validation on the training
+# records (gfx950_report.md lists the candidates with their held-out
+# regret).
 SCHEMA: List[Tuple[str, List[int]]] = [
+    ("query_rows", [1024, 4096]),
+    ("density", [700, 2000]),
+    ("run_coverage", [8000]),
+]
+# A candidate that adds row_imbalance = max_row_nnz * query_rows / nnz, the
+# longest row against the mean row (near 1 for top-k and window masks, well
+# above 1 when heads differ in density).
+IMBALANCE_SCHEMA: List[Tuple[str, List[int]]] = [
     ("query_rows", [1024, 4096]),
     ("density", [700, 2000]),
     ("run_coverage", [9000]),
@@ -53,9 +59,9 @@ SEQ_HEADS_SCHEMA: List[Tuple[str, List[int]]] = [
 
 # Profiling records the shipped table is built from, and held-out records.
 PROFILES = [os.path.join(HERE, "gfx950_profile.jsonl"), os.path.join(HERE, "gfx950_wide.jsonl"),
-            os.path.join(HERE, "gfx950_mixture.jsonl")]
+            os.path.join(HERE, "gfx950_mixture.jsonl"), os.path.join(HERE, "gfx950_large.jsonl")]
 EVALS = [os.path.join(HERE, "gfx950_eval.jsonl"), os.path.join(HERE, "gfx950_wide_eval.jsonl"),
-         os.path.join(HERE, "gfx950_mixture_eval.jsonl")]
+         os.path.join(HERE, "gfx950_mixture_eval.jsonl"), os.path.join(HERE, "gfx950_large_eval.jsonl")]
 
 
 def with_query_rows(rec: Dict) -> Dict:
@@ -134,13 +140,16 @@ def cv_regret(records: Sequence[Dict], schema, base_plan, folds: int = 4) -> flo
 # regret on the training records).
 CANDIDATE_SCHEMAS: List[List[Tuple[str, List[int]]]] = [
     SCHEMA,
+    IMBALANCE_SCHEMA,
     [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [9000]), ("row_imbalance", [25000])],
     [("query_rows", [512, 2048, 8192]), ("density", [700, 2000]), ("run_coverage", [9000]),
      ("row_imbalance", [30000])],
     [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [5000, 9000])],
     [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [9000])],
-    [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [8000])],
     [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [5000])],
+    [("query_rows", [1024, 4096, 16384]), ("density", [700, 2000]), ("run_coverage", [9000])],
+    [("query_rows", [1024, 4096, 32768]), ("density", [700, 2000]), ("run_coverage", [9000])],
+    [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [9000]), ("row_imbalance", [20000])],
     [("query_rows", [512, 2048, 8192]), ("density", [700, 2000]), ("run_coverage", [8000])],
     [("query_rows", [512, 2048, 8192]), ("density", [700, 2000]), ("run_coverage", [5000])],
     [("query_rows", [256, 1024, 4096, 16384]), ("density", [700, 2000]), ("run_coverage", [5000])],
@@ -368,9 +377,10 @@ def write_report(path: str, table, base, catalog, prof_recs, eval_recs, candidat
     pick = lambda r: table.get(tuple(r["key"]), {}).get(bucket(r["features"], SCHEMA), [base(tuple(r["key"]))])
     lines = ["# gfx950 plan table: selection quality on MI355X", "",
              "Generated by `python -m paper_2609_25869_amd.lut.compile --report` from the committed profiling "
-             "records: the table is built from `gfx950_profile.jsonl` and `gfx950_wide.jsonl`; "
-             "`gfx950_eval.jsonl` and `gfx950_wide_eval.jsonl` hold held-out cases of the same generators with "
+             "records: the table is built from %s; %s hold held-out cases of the same generators with "
              "other seeds.  Latencies are kernel times: the median of 3 timed batches after 1 warm-up launch, "
+             % (", ".join("`%s`" % os.path.basename(x) for x in PROFILES),
+                ", ".join("`%s`" % os.path.basename(x) for x in EVALS)) +
              "where a launch shorter than 1 ms is timed in batches of back-to-back launches of about 1 ms "
              "(HIP events around each batch).",
              "", "## Selector regret (selected / fastest measured latency per case)", "",
@@ -509,10 +519,12 @@ def main():
     args.out = args.out or os.path.join(HERE, "gfx950_v1.json")
     table = compile_table(recs, SCHEMA, base)
     prov = {"profiled_on": "MI355X (gfx950)", "profile_cases": len(recs),
-            "corpus": "seeded synthetic masks (frame windows, Bernoulli + diagonal, pooled q.k top-k) on the "
-                      "nine paper geometries + (128,32)/(32,128): the grid split (N in {16K, 64K, 115K}, 4 or 24 "
-                      "batch x heads, 6 sources) and the wide split (N from 2K to 115K, 1 to 24 batch x heads, "
-                      "12 sources, 96 random draws per key)",
+            "corpus": "seeded synthetic masks (frame windows, Bernoulli + diagonal, pooled q.k top-k, per-head "
+                      "mixtures) on the nine paper geometries + (128,32)/(32,128): the grid split (N in {16K, 64K, "
+                      "115K}, 4 or 24 batch x heads, 6 sources), the wide split (N from 2K to 115K, 1 to 24 batch "
+                      "x heads, 12 sources, 96 random draws per key), the mixture split (N from 16K to 131K, 8 to "
+                      "48 batch x heads, 12 draws per key) and the large split (N from 64K to 131K, 8 to 48 batch "
+                      "x heads, 12 sources and mixtures, 12 draws per key)",
             "latency": "median of 3 timed batches after 1 warm-up launch; launches under 1 ms timed as back-to-back batches of about 1 ms (HIP events)"}
     if all(os.path.exists(e) for e in args.eval):
         ev = load_records(args.eval)

@@ -21,7 +21,8 @@ Corpus (the paper's profiling masks are not available; these stand in):
   tokens; 4 or 24 (batch x heads); masks from three families at several
   densities -- frame-window masks (long runs, like spatiotemporal windows),
   Bernoulli masks with the diagonal (few runs) and per-row top-k of pooled
-  q.k block scores with the diagonal.  Inputs are N(0,1) in bf16.
+  q.k block scores with the diagonal.  Inputs are N(0,1) in bf16.  The
+  wide, mixture and large splits widen this grid (see their constants).
 
     python -m paper_2609_25869_amd.lut.profile --out PATH [--split profile|eval] [--budget SECONDS]
 """
@@ -39,7 +40,8 @@ SEQ_LENS = [16384, 65536, 115200]
 BATCH_HEADS = [4, 24]
 FAMILIES = [("window", 0.05), ("window", 0.15), ("bernoulli", 0.03), ("bernoulli", 0.10), ("bernoulli", 0.30),
             ("topk", 0.12)]
-SPLIT_SEED = {"profile": 0, "eval": 1, "wide": 2, "wide_eval": 3, "mixture": 4, "mixture_eval": 5}
+SPLIT_SEED = {"profile": 0, "eval": 1, "wide": 2, "wide_eval": 3, "mixture": 4, "mixture_eval": 5, "large": 6,
+              "large_eval": 7}
 FRAMES = 16
 
 # The wide splits draw, per request key, random combinations of a larger
@@ -61,6 +63,14 @@ MIX_PER_KEY = {"mixture": 12, "mixture_eval": 6}
 MIX_FAMILIES = [("window", 0.4), ("topk", 0.4), ("bernoulli", 0.2)]
 MIX_RHO = [0.02, 0.05, 0.10, 0.25, 0.50]
 
+# The large splits: the request sizes of video generation (64K to 131K
+# tokens, 8 to 48 batch x heads), each case drawing one of the twelve wide
+# sources or a per-head mixture (a quarter of the cases).
+LARGE_SEQ = [65536, 98304, 115200, 131072]
+LARGE_BH = [8, 16, 24, 48]
+LARGE_SOURCES = WIDE_SOURCES + [("mixture", 0.0)] * 4
+LARGE_PER_KEY = {"large": 12, "large_eval": 6}
+
 
 def log(msg):
     print("[profile] " + msg, flush=True)
@@ -76,6 +86,15 @@ def corpus(split):
             for _ in range(MIX_PER_KEY[split]):
                 cases.append(dict(id="%s-%d" % (split, len(cases)), geometry=list(geom), N=rng.choice(MIX_SEQ),
                                   bh=rng.choice(MIX_BH), family="mixture", rho=0.0, seed=rng.randrange(1 << 30)))
+        return cases
+    if split in LARGE_PER_KEY:
+        import random
+        rng = random.Random(1000 + SPLIT_SEED[split])
+        for geom in GEOMETRIES:
+            for _ in range(LARGE_PER_KEY[split]):
+                fam, rho = rng.choice(LARGE_SOURCES)
+                cases.append(dict(id="%s-%d" % (split, len(cases)), geometry=list(geom), N=rng.choice(LARGE_SEQ),
+                                  bh=rng.choice(LARGE_BH), family=fam, rho=rho, seed=rng.randrange(1 << 30)))
         return cases
     if split in WIDE_PER_KEY:
         import random
