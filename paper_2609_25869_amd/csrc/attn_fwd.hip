@@ -204,15 +204,16 @@ __device__ inline void block_sync() {
 }
 
 // Waves per SIMD the register budget is sized for: two for G = 1 with four
-// or more waves per workgroup; one for G = 2 (its accumulators and Q
-// fragments need the whole register file) and for the 2-wave T_Q = 64
-// workgroups, whose 64 KB rings let only two workgroups share a CU.
-template <int NWAVES, int G>
-constexpr int waves_per_simd() { return (G == 1 && NWAVES > 2) ? 2 : 1; }
+// or more waves per workgroup, and for 2-wave workgroups whose ring takes
+// at most 32 KB (four of them share a CU); one for G = 2 (its accumulators
+// and Q fragments need the whole register file) and for the 2-wave T_Q = 64
+// workgroups with 64 KB rings, of which only two share a CU.
+template <int NWAVES, int G, int TKV, int STAGES>
+constexpr int waves_per_simd() { return (G == 1 && (NWAVES > 2 || TKV * STAGES <= 64)) ? 2 : 1; }
 
 template <int NWAVES, int G, int TKV, int STAGES>
-__global__ __launch_bounds__(64 * NWAVES) __attribute__((amdgpu_waves_per_eu(waves_per_simd<NWAVES, G>(),
-                                                                               waves_per_simd<NWAVES, G>())))
+__global__ __launch_bounds__(64 * NWAVES)
+__attribute__((amdgpu_waves_per_eu(waves_per_simd<NWAVES, G, TKV, STAGES>(), waves_per_simd<NWAVES, G, TKV, STAGES>())))
 void attn_fwd_kernel(AttnArgs a) {
   using C = Cfg<NWAVES, G, TKV>;
   constexpr int kNKB = C::kNKB;
@@ -824,11 +825,14 @@ hipError_t launch_variant(const AttnArgs& a, hipStream_t s) {
 // with 64-key tiles eight waves of 32 rows.
 hipError_t launch_attention(int tq, int tkv, int waves, int stages, const AttnArgs& a, hipStream_t s) {
   if (tq == 64 && tkv == 32 && waves == 2 && stages == 4) return launch_variant<2, 1, 32, 4>(a, s);
+  if (tq == 64 && tkv == 32 && waves == 2 && stages == 2) return launch_variant<2, 1, 32, 2>(a, s);
   if (tq == 64 && tkv == 64 && waves == 2 && stages == 2) return launch_variant<2, 1, 64, 2>(a, s);
   if (tq == 128 && tkv == 32 && waves == 4 && stages == 4) return launch_variant<4, 1, 32, 4>(a, s);
+  if (tq == 128 && tkv == 32 && waves == 4 && stages == 2) return launch_variant<4, 1, 32, 2>(a, s);
   if (tq == 128 && tkv == 64 && waves == 4 && stages == 2) return launch_variant<4, 1, 64, 2>(a, s);
   if (tq == 256 && tkv == 32 && waves == 4 && stages == 8) return launch_variant<4, 2, 32, 8>(a, s);
   if (tq == 256 && tkv == 64 && waves == 8 && stages == 2) return launch_variant<8, 1, 64, 2>(a, s);
+  if (tq == 256 && tkv == 64 && waves == 8 && stages == 4) return launch_variant<8, 1, 64, 4>(a, s);
   return hipErrorInvalidValue;
 }
 

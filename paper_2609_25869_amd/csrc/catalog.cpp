@@ -30,6 +30,18 @@ std::vector<CatalogEntry> build_catalog() {
   // ids 24-29: the split-free tiles with every XCD on the same stretch of tasks
   for (int tq : tqs)
     for (int tkv : tkvs) out.push_back(CatalogEntry{id++, tq, tkv, 1, default_stages(tq, tkv), default_waves(tq, tkv), 8});
+  // ids 30-32: the other ring depth of three split-free tiles, XCD pairs.
+  // (64, 32) with two slots fits four workgroups per CU (two waves per SIMD
+  // instead of one, each load with one iteration to land instead of three);
+  // (128, 32) with two slots (the same occupancy, a shallower prefetch);
+  // (256, 64) with four slots (loads with three iterations to land).
+  out.push_back(CatalogEntry{id++, 64, 32, 1, 2, 2, 2});
+  out.push_back(CatalogEntry{id++, 128, 32, 1, 2, 4, 2});
+  out.push_back(CatalogEntry{id++, 256, 64, 1, 4, 8, 2});
+  // ids 33-34: the two-slot (64, 32) and (128, 32) with every XCD on the
+  // same stretch of tasks
+  out.push_back(CatalogEntry{id++, 64, 32, 1, 2, 2, 8});
+  out.push_back(CatalogEntry{id++, 128, 32, 1, 2, 4, 8});
   return out;
 }
 

@@ -36,9 +36,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 # records (gfx950_report.md lists the candidates with their held-out
 # regret).
 SCHEMA: List[Tuple[str, List[int]]] = [
-    ("query_rows", [1024, 4096]),
+    ("query_rows", [1024, 4096, 32768]),
     ("density", [700, 2000]),
-    ("run_coverage", [8000]),
+    ("run_coverage", [9000]),
 ]
 # A candidate that adds row_imbalance = max_row_nnz * query_rows / nnz, the
 # longest row against the mean row (near 1 for top-k and window masks, well
@@ -148,7 +148,7 @@ CANDIDATE_SCHEMAS: List[List[Tuple[str, List[int]]]] = [
     [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [9000])],
     [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [5000])],
     [("query_rows", [1024, 4096, 16384]), ("density", [700, 2000]), ("run_coverage", [9000])],
-    [("query_rows", [1024, 4096, 32768]), ("density", [700, 2000]), ("run_coverage", [9000])],
+    [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [8000])],
     [("query_rows", [1024, 4096]), ("density", [700, 2000]), ("run_coverage", [9000]), ("row_imbalance", [20000])],
     [("query_rows", [512, 2048, 8192]), ("density", [700, 2000]), ("run_coverage", [8000])],
     [("query_rows", [512, 2048, 8192]), ("density", [700, 2000]), ("run_coverage", [5000])],
@@ -301,7 +301,7 @@ def kernel_ablations(pick, base_plan, catalog, records) -> Dict:
     given separately over the keys whose base plan is Direct and over the
     others (whose base plan is the nearest tile).  O0 / O1 / O2 hold the
     physical tile at the base plan's tile and vary only the task
-    organization (Split-K factor and traversal order): the base organization,
+    organization (Split-K factor, traversal order and ring depth): the base organization,
     the table's first-ranked plan with that tile, and the fastest measured
     one.  Paired-case geometric means; wins / ties / losses against O0 use a
     3% tie band.
@@ -433,7 +433,8 @@ def write_report(path: str, table, base, catalog, prof_recs, eval_recs, candidat
               "| A2: plan-table selection | %.3f | %.3f | %.3f |" % (
                   ab["kernel_speedup_over_A0"]["A2_table"], bk["direct"]["A2_table"], bk["nearest_tile"]["A2_table"]),
               "", "A2 / A1 kernel time: %.4f." % ab["A2_regret_vs_A1"], "",
-              "Task organization at the base tile (Split-K factor and traversal order vary, the tile does not):",
+              "Task organization at the base tile (Split-K factor, traversal order and ring depth vary, the tile "
+              "does not):",
               "",
               "| variant | speedup over O0 | regret vs O2 |", "|---|---:|---:|",
               "| O0: base organization (no split) | 1.000 | %.4f |" % o["O0_regret_vs_O2"],

@@ -212,7 +212,7 @@ def reference_rows(torch, q, k, v, mask, bq, bkv, rows):
     return out
 
 
-def profile_case(torch, bsa, case, reps=3):
+def profile_case(torch, bsa, case, reps=3, only=None):
     bq, bkv = case["geometry"]
     N, bh = case["N"], case["bh"]
     dev = torch.device("cuda")
@@ -230,6 +230,8 @@ def profile_case(torch, bsa, case, reps=3):
     base = bsa.base_plan(bq, bkv)
     plans = [e["id"] for e in bsa.catalog() if bsa.plan_eligible(e["id"], bq, bkv, shapes)]
     plans = [base] + [p for p in plans if p != base]
+    if only is not None:
+        plans = [p for p in plans if p in only]
     rng = torch.Generator()
     rng.manual_seed(case["seed"] + 11)
     rows = [(int(h), int(i)) for h, i in zip(torch.randint(0, bh, (64,), generator=rng).tolist(),
@@ -306,6 +308,95 @@ def refeature(args):
     log("refeatured %d records of %s in %.1f s" % (len(recs), args.split, time.time() - t0))
 
 
+def add_plans(args):
+    """Time plans added to the catalog after a split was profiled, and merge
+    them into its records (--base, written to --out).  Every case re-times
+    its recorded fastest plan and its base plan beside the new ones and keeps
+    the geometric mean of recorded / re-timed over those reference plans
+    (`scale`) with the new plans' raw latencies; `finalize_added` then puts
+    the new latencies on the clock the split was first profiled at.  The
+    regenerated mask must give the recorded statistics."""
+    import torch
+    import paper_2609_25869_amd as bsa
+    new = [int(x) for x in args.add_plans.split(",")]
+    by_id = {c["id"]: c for c in corpus(args.split)}
+    recs = [json.loads(l) for l in open(args.base) if l.strip()]
+    done = set()
+    if os.path.exists(args.out):
+        done = {json.loads(l)["id"] for l in open(args.out) if l.strip()}
+    todo = [r for r in recs if r["id"] not in done]
+    log("%d cases to extend with plans %s (%d already in %s)" % (len(todo), new, len(done), args.out))
+    t0 = time.time()
+    with open(args.out, "a") as f:
+        for i, rec in enumerate(todo):
+            if time.time() - t0 > args.budget:
+                log("budget reached after %d cases" % i)
+                break
+            tc = time.time()
+            case = by_id[rec["id"]]
+            old = rec["latency_ms"]
+            refs = sorted({min(old, key=old.get), str(bsa.base_plan(*case["geometry"]))} & set(old), key=int)
+            r = profile_case(torch, bsa, case, only=set(new) | {int(p) for p in refs})
+            assert all(r["features"][k] == v for k, v in rec["features"].items()), (rec["id"], rec["features"])
+            got = [old[p] / r["latency_ms"][p] for p in refs if p in r["latency_ms"]]
+            scale = math.exp(sum(math.log(x) for x in got) / len(got)) if got else 1.0
+            raw = {}
+            for p in new:
+                if str(p) in r["latency_ms"]:
+                    raw[str(p)] = r["latency_ms"][str(p)]
+                    old[str(p)] = raw[str(p)] * scale
+                elif p in r["invalid"] and p not in rec["invalid"]:
+                    rec["invalid"].append(p)
+            entry = {"plans": new, "refs": [int(p) for p in refs], "scale": scale, "raw": raw,
+                     "ref_ms": min(old[p] for p in refs) if refs else 0.0}
+            prev = rec.get("added")
+            rec["added"] = (prev if isinstance(prev, list) else [prev] if prev else []) + [entry]
+            f.write(json.dumps(rec) + "\n")
+            f.flush()
+            log("%s: scale %.4f, %s (%.1f s)" % (rec["id"], scale, ", ".join(
+                "%d %.3f" % (p, old[str(p)]) for p in new if str(p) in old), time.time() - tc))
+            torch.cuda.empty_cache()
+    log("done in %.1f s" % (time.time() - t0))
+
+
+FINALIZE_MIN_MS = 0.5
+
+
+def finalize_added(path):
+    """One clock factor per pass of --add-plans over a split (one pass runs on
+    one box): the geometric mean of the per-case reference ratios over the
+    cases whose reference kernels take at least FINALIZE_MIN_MS, where timing
+    noise is small.  Each added latency becomes its raw time times that
+    factor; per-case ratios of short kernels are too noisy to scale by alone.
+    Entries written before raw times were kept carry them implicitly as the
+    stored latency divided by the per-case scale."""
+    recs = [json.loads(l) for l in open(path) if l.strip()]
+    npass = max((len(r["added"]) if isinstance(r.get("added"), list) else 1) for r in recs)
+    for k in range(npass):
+        logs = []
+        for r in recs:
+            e = r["added"][k] if isinstance(r["added"], list) else r["added"]
+            ref_ms = e.get("ref_ms")
+            if ref_ms is None:
+                ref_ms = min(r["latency_ms"][str(p)] for p in e["refs"]) if e["refs"] else 0.0
+                e["ref_ms"] = ref_ms
+            if ref_ms >= FINALIZE_MIN_MS and e["scale"] > 0:
+                logs.append(math.log(e["scale"]))
+        factor = math.exp(sum(logs) / len(logs)) if logs else 1.0
+        for r in recs:
+            e = r["added"][k] if isinstance(r["added"], list) else r["added"]
+            if "raw" not in e:
+                e["raw"] = {str(p): r["latency_ms"][str(p)] / e["scale"] for p in e["plans"] if str(p) in r["latency_ms"]}
+            for p, t in e["raw"].items():
+                r["latency_ms"][p] = t * factor
+            e["factor"] = factor
+        log("%s pass %d: factor %.4f from %d of %d cases" % (path, k, factor, len(logs), len(recs)))
+    with open(path + ".tmp", "w") as f:
+        for r in recs:
+            f.write(json.dumps(r) + "\n")
+    os.replace(path + ".tmp", path)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", required=True)
@@ -314,9 +405,20 @@ def main():
     ap.add_argument("--only", default="", help="comma-separated geometries 'bq:bkv' to profile")
     ap.add_argument("--refeature", action="store_true",
                     help="only add the max_row_nnz statistic to the existing records in --out (no timing)")
+    ap.add_argument("--add-plans", default="",
+                    help="comma-separated catalog ids to time and merge into the records of --base")
+    ap.add_argument("--base", default="", help="records of --split to extend (with --add-plans)")
+    ap.add_argument("--finalize", action="store_true",
+                    help="put the plans added to the records in --out on one clock factor per pass (no timing)")
     args = ap.parse_args()
+    if args.finalize:
+        finalize_added(args.out)
+        return
     if args.refeature:
         refeature(args)
+        return
+    if args.add_plans:
+        add_plans(args)
         return
     import torch
     import paper_2609_25869_amd as bsa

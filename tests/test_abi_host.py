@@ -64,9 +64,11 @@ def test_catalog_layout():
     """Every catalog entry names the kernel that runs it: wavefronts and ring
     depth as launched (one wave per 32 query rows and 64 KB rings, except
     T = (256, 32), four waves of 64 rows with an eight-slot ring); ids 24-29
-    repeat the split-free tiles with the all-XCD traversal order."""
+    repeat the split-free tiles with the all-XCD traversal order; ids 30-32
+    are the other ring depth of (64, 32), (128, 32) and (256, 64) (XCD pairs),
+    ids 33-34 the first two of those with the all-XCD order."""
     cat = bsa.catalog()
-    assert len(cat) == 30
+    assert len(cat) == 35
     tqs, tkvs, splits = (64, 128, 256), (32, 64), (1, 2, 4, 8)
 
     def launched(tq, tkv):
@@ -82,7 +84,10 @@ def test_catalog_layout():
         assert (e["stages"], e["waves"]) == launched(e["tq"], e["tkv"])
     # the (256, 32) plans run four 64-row waves through an eight-slot ring
     assert [(e["stages"], e["waves"]) for e in cat[16:20]] == [(8, 4)] * 4
-    st = bsa._lib.bsa_catalog_get(30, ctypes.byref(_ffi.CatalogEntry()))
+    assert [(e["id"], e["tq"], e["tkv"], e["split"], e["stages"], e["waves"], e["xcd_group"]) for e in cat[30:]] == [
+        (30, 64, 32, 1, 2, 2, 2), (31, 128, 32, 1, 2, 4, 2), (32, 256, 64, 1, 4, 8, 2),
+        (33, 64, 32, 1, 2, 2, 8), (34, 128, 32, 1, 2, 4, 8)]
+    st = bsa._lib.bsa_catalog_get(35, ctypes.byref(_ffi.CatalogEntry()))
     assert st == _ffi.BSA_ERR_INVALID
 
 
