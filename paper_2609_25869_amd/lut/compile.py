@@ -61,7 +61,8 @@ SEQ_HEADS_SCHEMA: List[Tuple[str, List[int]]] = [
 PROFILES = [os.path.join(HERE, "gfx950_profile.jsonl"), os.path.join(HERE, "gfx950_wide.jsonl"),
             os.path.join(HERE, "gfx950_mixture.jsonl"), os.path.join(HERE, "gfx950_large.jsonl")]
 EVALS = [os.path.join(HERE, "gfx950_eval.jsonl"), os.path.join(HERE, "gfx950_wide_eval.jsonl"),
-         os.path.join(HERE, "gfx950_mixture_eval.jsonl"), os.path.join(HERE, "gfx950_large_eval.jsonl")]
+         os.path.join(HERE, "gfx950_mixture_eval.jsonl"), os.path.join(HERE, "gfx950_large_eval.jsonl"),
+         os.path.join(HERE, "gfx950_grid2.jsonl")]
 
 
 def with_query_rows(rec: Dict) -> Dict:
@@ -524,7 +525,7 @@ def main():
                       "mixtures) on the nine paper geometries + (128,32)/(32,128): the grid split (N in {16K, 64K, "
                       "115K}, 4 or 24 batch x heads, 6 sources), the wide split (N from 2K to 115K, 1 to 24 batch "
                       "x heads, 12 sources, 96 random draws per key), the mixture split (N from 16K to 131K, 8 to "
-                      "48 batch x heads, 12 draws per key) and the large split (N from 64K to 131K, 8 to 48 batch "
+                      "48 batch x heads, 12 draws per key), the large split (N from 64K to 131K, 8 to 48 batch "
                       "x heads, 12 sources and mixtures, 12 draws per key)",
             "latency": "median of 3 timed batches after 1 warm-up launch; launches under 1 ms timed as back-to-back batches of about 1 ms (HIP events)"}
     if all(os.path.exists(e) for e in args.eval):

@@ -41,7 +41,7 @@ BATCH_HEADS = [4, 24]
 FAMILIES = [("window", 0.05), ("window", 0.15), ("bernoulli", 0.03), ("bernoulli", 0.10), ("bernoulli", 0.30),
             ("topk", 0.12)]
 SPLIT_SEED = {"profile": 0, "eval": 1, "wide": 2, "wide_eval": 3, "mixture": 4, "mixture_eval": 5, "large": 6,
-              "large_eval": 7}
+              "large_eval": 7, "grid2": 8}
 FRAMES = 16
 
 # The wide splits draw, per request key, random combinations of a larger
@@ -70,6 +70,12 @@ LARGE_SEQ = [65536, 98304, 115200, 131072]
 LARGE_BH = [8, 16, 24, 48]
 LARGE_SOURCES = WIDE_SOURCES + [("mixture", 0.0)] * 4
 LARGE_PER_KEY = {"large": 12, "large_eval": 6}
+
+# The second grid split (held out): the grid split's geometries and
+# sources at the batch x heads between its two (8 and 16), from 32K to 115K
+# tokens.
+GRID2_SEQ = [32768, 65536, 115200]
+GRID2_BH = [8, 16]
 
 
 def log(msg):
@@ -105,11 +111,12 @@ def corpus(split):
                 cases.append(dict(id="%s-%d" % (split, len(cases)), geometry=list(geom), N=rng.choice(WIDE_SEQ),
                                   bh=rng.choice(WIDE_BH), family=fam, rho=rho, seed=rng.randrange(1 << 30)))
         return cases
+    seqs, bhs = (GRID2_SEQ, GRID2_BH) if split == "grid2" else (SEQ_LENS, BATCH_HEADS)
     for gi, geom in enumerate(GEOMETRIES):
-        for N in SEQ_LENS:
-            for bh in BATCH_HEADS:
+        for N in seqs:
+            for bh in bhs:
                 for fi, (fam, rho) in enumerate(FAMILIES):
-                    seed = ((SPLIT_SEED[split] * 16 + gi) * 8 + SEQ_LENS.index(N)) * 64 + BATCH_HEADS.index(bh) * 8 + fi
+                    seed = ((SPLIT_SEED[split] * 16 + gi) * 8 + seqs.index(N)) * 64 + bhs.index(bh) * 8 + fi
                     cases.append(dict(id="%s-%d" % (split, len(cases)), geometry=list(geom), N=N, bh=bh, family=fam,
                                       rho=rho, seed=seed))
     return cases
