@@ -127,7 +127,8 @@ typedef struct {
   int32_t xcd_group; /* traversal order: the MI355X's eight XCDs work in groups of this many (2 or 8), each
                         group through its own contiguous share of the dispatch order, the XCDs of a group
                         taking turns over runs of 8 consecutive tasks; 8 keeps every XCD on the same stretch
-                        of tasks (the same heads), 2 spreads four stretches over the chip */
+                        of tasks (the same heads), 2 spreads four stretches over the chip.  Without Split-K
+                        the shares hold equal work (per-(b, h) active blocks), otherwise equal task counts */
 } bsa_catalog_entry;
 
 /* Regime-lookup input z_A(R) = <k_A(R), u_A(R), s_A(M)> (Eq. 3).  Tables

@@ -126,6 +126,9 @@ struct AttnArgs {
   int32_t gq, gkv;              // membership grid of a tile
   float scale_log2;             // log2(e) / sqrt(d)
   int32_t slot_group, slot_run; // launch-slot to task map: XCDs per group (1, 2, 4 or 8) and run length
+  int32_t balanced;             // nonzero: group g's share of the task list is [share_lo[g], share_lo[g + 1])
+  int32_t share_lo[5];
+  int64_t nslots;               // launch slots (0: the task count rounded up to 8)
 };
 
 // Kernel launchers (defined in the .hip files).

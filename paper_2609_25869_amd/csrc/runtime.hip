@@ -185,7 +185,49 @@ struct Segment {
   int32_t* dispatch = nullptr;  // the dispatch order (exported); null: row order
   float* ws = nullptr;
   int64_t ws_bytes = 0;
+  // split-free plans whose XCDs work in groups: the groups' shares of the
+  // task list, cut to hold equal work, and the launch slots they need
+  bool balanced = false;
+  int32_t share_lo[5] = {0, 0, 0, 0, 0};
+  int64_t nslots = 0;
 };
+
+// Shares of the XCD groups over a split-free task list: contiguous
+// stretches holding equal work.  The task list holds npq tasks per (b, h) in
+// (b, head) order, whatever the dispatch order does inside a head; a head's
+// work (its active logical blocks) is taken as spread evenly over its tasks,
+// so a cut may fall inside a head.  Requests whose heads carry equal work
+// keep equal task counts.  Fills lo[0..4] (lo[g] = nt past the last group)
+// and the launch slots the shares need (the map of task_of_slot).
+void balanced_shares(const std::vector<int64_t>& work, int64_t npq, int32_t group, int32_t run, int32_t* lo,
+                     int64_t* nslots) {
+  const int ngroups = 8 / group;
+  const int64_t nbh = (int64_t)work.size(), nt = nbh * npq;
+  std::vector<int64_t> cw(nbh + 1, 0);
+  for (int64_t k = 0; k < nbh; ++k) cw[k + 1] = cw[k] + work[k];
+  const int64_t total = cw[nbh];
+  for (int g = 0; g <= 4; ++g) lo[g] = (int32_t)nt;
+  lo[0] = 0;
+  for (int g = 1; g < ngroups; ++g) {
+    int64_t pos;
+    if (total == 0) {
+      pos = (nt * g + ngroups - 1) / ngroups;
+    } else {
+      const int64_t target = total * g / ngroups;
+      int64_t k = 0;
+      while (k + 1 < nbh && cw[k + 1] <= target) ++k;
+      pos = k * npq + (work[k] > 0 ? ((target - cw[k]) * npq + work[k] / 2) / work[k] : 0);
+    }
+    lo[g] = (int32_t)std::min<int64_t>(nt, std::max<int64_t>(pos, lo[g - 1]));
+  }
+  int64_t most = 0;
+  for (int g = 0; g < ngroups; ++g) {
+    const int64_t n = (int64_t)lo[g + 1] - lo[g], whole = n / ((int64_t)group * run);
+    const int64_t r = n - whole * group * run;
+    most = std::max<int64_t>(most, whole * run + (r + group - 1) / group);
+  }
+  *nslots = 8 * most;
+}
 
 }  // namespace
 
@@ -552,11 +594,13 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
   p->scan_tmp_dev = reinterpret_cast<int64_t*>(pre8 + o_scan);
 
   std::vector<SegStats> stats(nseg);
+  std::vector<unsigned long long> bh_nnz;
   {
     Staging& stg = staging();
     std::lock_guard<std::mutex> lk(stg.mu);
     const size_t stats_at = align256(upload_bytes);
-    if ((st = stg.reserve(stats_at + sizeof(SegStats) * nseg)) != BSA_OK) return st;
+    const size_t bhnnz_at = align256(stats_at + sizeof(SegStats) * nseg);
+    if ((st = stg.reserve(bhnnz_at + sizeof(unsigned long long) * (size_t)B * H)) != BSA_OK) return st;
     uint8_t* h8 = static_cast<uint8_t*>(stg.ptr);
     std::memset(h8, 0, upload_bytes);
     std::memcpy(h8 + o_heads, p->heads.data(), sizeof(HeadDesc) * H);
@@ -583,10 +627,15 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
     ma.bh_nnz = p->bh_nnz_dev;
     HIP_TRY(launch_mask_count(ma, stream));
     HIP_TRY(launch_scan_i32(p->counts_dev, p->row_ptr_dev, p->R, p->scan_tmp_dev, stream));
-    // the request's single device-to-host copy: the scalar statistics
+    // the request's single synchronisation: the segment statistics and the
+    // per-(b, h) active block counts
     HIP_TRY(hipMemcpyAsync(h8 + stats_at, p->stats_dev, sizeof(SegStats) * nseg, hipMemcpyDeviceToHost, stream));
+    HIP_TRY(hipMemcpyAsync(h8 + bhnnz_at, p->bh_nnz_dev, sizeof(unsigned long long) * (size_t)B * H,
+                           hipMemcpyDeviceToHost, stream));
     HIP_TRY(hipStreamSynchronize(stream));
     std::memcpy(stats.data(), h8 + stats_at, sizeof(SegStats) * nseg);
+    bh_nnz.resize((size_t)B * H);
+    std::memcpy(bh_nnz.data(), h8 + bhnnz_at, sizeof(unsigned long long) * (size_t)B * H);
   }
 
   // ---- regime lookup and ranked fallback per segment (host)
@@ -612,6 +661,13 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
       return fail(BSA_ERR_UNSUPPORTED, "too many active tiles for 32-bit tile indices");
     sg.tasks_bound = e.split == 1 ? sg.Rp : std::min(sg.Rp * e.split, sg.Rp + sg.tiles_bound);
     if (sg.tasks_bound >= INT32_MAX) return fail(BSA_ERR_UNSUPPORTED, "too many tasks for one launch");
+    sg.balanced = e.split == 1 && (e.xcd_group == 2 || e.xcd_group == 4);
+    if (sg.balanced) {
+      std::vector<int64_t> work;
+      for (int b = 0; b < B; ++b)
+        for (int32_t h : sg.heads) work.push_back((int64_t)bh_nnz[(size_t)b * H + h]);
+      balanced_shares(work, sg.npq, e.xcd_group, kSlotRun, sg.share_lo, &sg.nslots);
+    }
   }
   if (p->nnz >= INT32_MAX) return fail(BSA_ERR_UNSUPPORTED, "too many active blocks");
 
@@ -795,6 +851,9 @@ bsa_status bsa_forward(bsa_plan_t plan, const void* q, const void* k, const void
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)s.head_dim));
     a.slot_group = e.xcd_group;
     a.slot_run = kSlotRun;
+    a.balanced = sg.balanced ? 1 : 0;
+    for (int g = 0; g < 5; ++g) a.share_lo[g] = sg.share_lo[g];
+    a.nslots = sg.nslots;
     HIP_TRY(launch_attention(e.tq, e.tkv, e.waves, e.stages, a, stream));
     if (e.split > 1) HIP_TRY(launch_splitk_merge(e.tq, a, stream));
   }
