@@ -600,6 +600,7 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
     std::lock_guard<std::mutex> lk(stg.mu);
     const size_t stats_at = align256(upload_bytes);
     const size_t bhnnz_at = align256(stats_at + sizeof(SegStats) * nseg);
+    if (bhnnz_at - stats_at != o_bhnnz - o_stats) return fail(BSA_ERR_HIP, "statistics staging layout");
     if ((st = stg.reserve(bhnnz_at + sizeof(unsigned long long) * (size_t)B * H)) != BSA_OK) return st;
     uint8_t* h8 = static_cast<uint8_t*>(stg.ptr);
     std::memset(h8, 0, upload_bytes);
@@ -629,8 +630,10 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
     HIP_TRY(launch_scan_i32(p->counts_dev, p->row_ptr_dev, p->R, p->scan_tmp_dev, stream));
     // the request's single synchronisation: the segment statistics and the
     // per-(b, h) active block counts
-    HIP_TRY(hipMemcpyAsync(h8 + stats_at, p->stats_dev, sizeof(SegStats) * nseg, hipMemcpyDeviceToHost, stream));
-    HIP_TRY(hipMemcpyAsync(h8 + bhnnz_at, p->bh_nnz_dev, sizeof(unsigned long long) * (size_t)B * H,
+    // (one copy: both buffers start 256-aligned and lie at the same distance
+    // apart on the device and in the staging buffer)
+    static_assert(sizeof(SegStats) % 8 == 0, "statistics layout");
+    HIP_TRY(hipMemcpyAsync(h8 + stats_at, p->stats_dev, (o_bhnnz - o_stats) + sizeof(unsigned long long) * (size_t)B * H,
                            hipMemcpyDeviceToHost, stream));
     HIP_TRY(hipStreamSynchronize(stream));
     std::memcpy(stats.data(), h8 + stats_at, sizeof(SegStats) * nseg);
