@@ -25,6 +25,12 @@ Corpus (the paper's profiling masks are not available; these stand in):
   wide, mixture and large splits widen this grid (see their constants).
 
     python -m paper_2609_25869_amd.lut.profile --out PATH [--split profile|eval] [--budget SECONDS]
+
+Plans added to the catalog later (or whose launch changed) are timed into
+existing records and then put on each split's original clock:
+
+    python -m paper_2609_25869_amd.lut.profile --split S --add-plans 30,31 --base gfx950_S.jsonl --out NEW
+    python -m paper_2609_25869_amd.lut.profile --out NEW --finalize
 """
 from __future__ import annotations
 
