@@ -28,6 +28,7 @@ PEAK_HBM_GBS = 8000.0
 FLUSH_BYTES = 512 << 20
 KERNEL_SRC = os.path.join(HERE, "paper_2609_25869_amd", "csrc", "attn_fwd.hip")
 ORDER_SRC = os.path.join(HERE, "paper_2609_25869_amd", "csrc", "task_order.hip")  # dispatch order: sets L2 reuse
+SLOTMAP_SRC = os.path.join(HERE, "paper_2609_25869_amd", "csrc", "slot_map.h")  # which XCD runs which task
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "attn_fwd_c2_window15_traffic.md")
 
 
@@ -88,7 +89,7 @@ def measured_traffic(workload, plan_ids):
     """HBM bytes per launch of the attention kernel from the committed counter summary.
 
     Reported only when that summary was taken on this workload and plan with
-    the current kernel and dispatch-order sources; otherwise None.
+    the current kernel, slot-map and dispatch-order sources; otherwise None.
     """
     import hashlib
     if not os.path.exists(TRAFFIC_FILE):
@@ -100,8 +101,9 @@ def measured_traffic(workload, plan_ids):
     rec = json.loads(text[a + 7:text.index("```", a + 7)])
     src_hash = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
     order_hash = hashlib.sha256(open(ORDER_SRC, "rb").read()).hexdigest()
+    slot_hash = hashlib.sha256(open(SLOTMAP_SRC, "rb").read()).hexdigest()
     if rec.get("workload") != workload or rec.get("plan_ids") != plan_ids or rec.get("attn_fwd_sha256") != src_hash \
-            or rec.get("task_order_sha256") != order_hash:
+            or rec.get("task_order_sha256") != order_hash or rec.get("slot_map_sha256") != slot_hash:
         return None
     return rec["hbm_bytes_per_launch"]
 

@@ -45,6 +45,7 @@
 // any of this; a row whose reference is still unset uses 0 as its
 // reference, so no NaN can arise (it keeps l = 0 and O = 0).
 #include "bsa_internal.h"
+#include "slot_map.h"
 
 namespace bsa {
 
@@ -117,50 +118,6 @@ struct Cfg {
   static constexpr int kNKB = TKV / 32;                 // 32-key blocks per tile
   static constexpr int kTileBytes = TKV * kRowBytes;
 };
-
-// Map the launch slot to a task.  Slot i runs on XCD i % 8.  The XCDs form
-// 8 / group groups of `group` XCDs; group g works through the g-th contiguous
-// share of the task list, and inside it its XCDs take turns over runs of
-// `run` consecutive tasks (XCD member m takes runs m, m + group, ...), so
-// neighbouring tasks still share an XCD while the group's XCDs stay on the
-// same stretch of the list.  group = 1 gives each XCD its own contiguous
-// eighth; group = 8 keeps all XCDs on one stretch.  The shares are equal in
-// task count, or given (share_lo non-null: group g takes [share_lo[g],
-// share_lo[g + 1]), cut by the planner so that the shares hold equal work).
-// The tail of a share that does not fill whole rounds of runs is dealt out
-// one task per XCD.  Slots map one-to-one onto [0, nt), the rest to -1.
-__device__ inline int64_t task_of_slot(int64_t slot, int64_t nt, int64_t group, int64_t run,
-                                       const int32_t* share_lo) {
-  const int64_t xcd = slot & 7, local = slot >> 3;
-  if (group <= 1) {
-    const int64_t per = (nt + 7) / 8;
-    const int64_t t = xcd * per + local;
-    return (local < per && t < nt) ? t : -1;
-  }
-  const int64_t ngroups = 8 / group, gi = xcd / group, mi = xcd % group;
-  int64_t lo, n;
-  if (share_lo) {
-    // a select over the (at most four) groups keeps the bounds in scalar
-    // registers; an indexed read would place the argument array in scratch
-    int64_t a0 = 0, a1 = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (i == gi) {
-        a0 = share_lo[i];
-        a1 = share_lo[i + 1];
-      }
-    lo = a0;
-    n = a1 - a0;
-  } else {
-    const int64_t per = (nt + ngroups - 1) / ngroups;
-    lo = gi * per;
-    n = min(nt, lo + per) - lo;
-  }
-  const int64_t whole = n / (group * run);  // complete rounds of runs
-  const int64_t t = local < whole * run ? (local / run) * group * run + mi * run + local % run
-                                        : whole * group * run + (local - whole * run) * group + mi;
-  return t < n ? lo + t : -1;
-}
 
 // Value of the same register in lane l ^ 32 (the other half of the wave).
 __device__ inline uint32_t other_half_u32(uint32_t x) {
@@ -828,7 +785,7 @@ __global__ __launch_bounds__(256) void splitk_merge_kernel(AttnArgs a) {
 
 template <int NWAVES, int G, int TKV, int STAGES>
 hipError_t launch_variant(const AttnArgs& a, hipStream_t s) {
-  const int64_t slots = a.nslots > 0 ? a.nslots : ((int64_t)a.ntasks + 7) / 8 * 8;
+  const int64_t slots = a.nslots > 0 ? a.nslots : default_slots(a.ntasks);
   if (slots == 0) return hipSuccess;
   hipLaunchKernelGGL((attn_fwd_kernel<NWAVES, G, TKV, STAGES>), dim3((unsigned)slots), dim3(64 * NWAVES), 0, s, a);
   return hipGetLastError();

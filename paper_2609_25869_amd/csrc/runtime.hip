@@ -21,6 +21,7 @@
 #include "../../include/bsa.h"
 #include "bsa_internal.h"
 #include "catalog.h"
+#include "slot_map.h"
 
 using namespace bsa;
 
@@ -191,43 +192,6 @@ struct Segment {
   int32_t share_lo[5] = {0, 0, 0, 0, 0};
   int64_t nslots = 0;
 };
-
-// Shares of the XCD groups over a split-free task list: contiguous
-// stretches holding equal work.  The task list holds npq tasks per (b, h) in
-// (b, head) order, whatever the dispatch order does inside a head; a head's
-// work (its active logical blocks) is taken as spread evenly over its tasks,
-// so a cut may fall inside a head.  Requests whose heads carry equal work
-// keep equal task counts.  Fills lo[0..4] (lo[g] = nt past the last group)
-// and the launch slots the shares need (the map of task_of_slot).
-void balanced_shares(const std::vector<int64_t>& work, int64_t npq, int32_t group, int32_t run, int32_t* lo,
-                     int64_t* nslots) {
-  const int ngroups = 8 / group;
-  const int64_t nbh = (int64_t)work.size(), nt = nbh * npq;
-  std::vector<int64_t> cw(nbh + 1, 0);
-  for (int64_t k = 0; k < nbh; ++k) cw[k + 1] = cw[k] + work[k];
-  const int64_t total = cw[nbh];
-  for (int g = 0; g <= 4; ++g) lo[g] = (int32_t)nt;
-  lo[0] = 0;
-  for (int g = 1; g < ngroups; ++g) {
-    int64_t pos;
-    if (total == 0) {
-      pos = (nt * g + ngroups - 1) / ngroups;
-    } else {
-      const int64_t target = total * g / ngroups;
-      int64_t k = 0;
-      while (k + 1 < nbh && cw[k + 1] <= target) ++k;
-      pos = k * npq + (work[k] > 0 ? ((target - cw[k]) * npq + work[k] / 2) / work[k] : 0);
-    }
-    lo[g] = (int32_t)std::min<int64_t>(nt, std::max<int64_t>(pos, lo[g - 1]));
-  }
-  int64_t most = 0;
-  for (int g = 0; g < ngroups; ++g) {
-    const int64_t n = (int64_t)lo[g + 1] - lo[g], whole = n / ((int64_t)group * run);
-    const int64_t r = n - whole * group * run;
-    most = std::max<int64_t>(most, whole * run + (r + group - 1) / group);
-  }
-  *nslots = 8 * most;
-}
 
 }  // namespace
 
@@ -669,7 +633,8 @@ bsa_status bsa_plan(const bsa_mask* mask, const int32_t* B_Q, const int32_t* B_K
       std::vector<int64_t> work;
       for (int b = 0; b < B; ++b)
         for (int32_t h : sg.heads) work.push_back((int64_t)bh_nnz[(size_t)b * H + h]);
-      balanced_shares(work, sg.npq, e.xcd_group, kSlotRun, sg.share_lo, &sg.nslots);
+      balanced_shares(work, sg.npq, e.xcd_group, sg.share_lo);
+      sg.nslots = shares_slots(sg.share_lo, e.xcd_group, kSlotRun);
     }
   }
   if (p->nnz >= INT32_MAX) return fail(BSA_ERR_UNSUPPORTED, "too many active blocks");
